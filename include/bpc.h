@@ -1,0 +1,209 @@
+/*
+ * bpc.h -- C ABI of the BinaryPC decode hot path on AMD Instinct MI355X
+ * (gfx950).
+ *
+ * BinaryPC ("Training-Free Hashing-Based Attention via Binary Principal
+ * Components") approximates every cached key k by h P, with a binary code
+ * h in {-1,+1}^L and a real projection P [L, D] (Sec. 3.2, Problem
+ * Formulation).  At prefill, P and the codes are built greedily from the
+ * keys (Algorithm "Constructing hash codes and corresponding hashing
+ * projection"), or keys are hashed against a given P (Algorithm "Given
+ * projection, computing hashcode").  At decode, the query is projected to
+ * q P^T, quantised to 7-bit magnitudes and packed into bit planes; every
+ * cached code is scored with XOR and popcount (Algorithm "Computing hashing
+ * score", Appendix "CUDA Optimizations on Bitwise Operations"); the top-k
+ * keys are selected and softmax attention runs over the gathered K/V rows
+ * only (Sec. 4.2, Kernel Evaluation).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - All tensor pointers are DEVICE pointers owned by the caller.  The
+ *   library never allocates device memory; scratch space is passed in as a
+ *   caller-owned workspace whose size the *_workspace_bytes functions give.
+ * - bf16 tensors are passed as `const uint16_t*` bit patterns.
+ * - Strides are in elements of the pointed-to type; the innermost
+ *   dimension (D for K, V, q, P; the W code words of one key) is contiguous.
+ * - Shapes: B sequences, Hq query heads, Hkv KV heads (Hq = G Hkv with the
+ *   group size G in {1, 2, 4, 8, 16}; query head j reads KV head j / G),
+ *   N cached keys, D = 128 head dim,
+ *   L in {32, 64, 128} code bits, W = L / 32 words per code.
+ * - Code bit i of a key is bit (i % 32) of 32-bit word i / 32; a set bit
+ *   means h_i = +1.
+ * - Calls are asynchronous on `stream` (a hipStream_t; NULL = the default
+ *   stream).  All argument checks happen on the host before anything is
+ *   enqueued: on error nothing is launched and no output is touched.
+ *   Faults during kernel execution surface at the caller's next sync.
+ * - Pointers must be 16-byte aligned and row strides multiples of 8
+ *   elements (16 bytes), else BPC_EALIGN.
+ * - Calls share no mutable state except a thread-local error message, so
+ *   they are reentrant; two calls that share an output or a workspace must
+ *   not overlap in time.
+ * - Arithmetic that decides a code bit is IEEE binary64 in a fixed order:
+ *   dot products over D split D into 4 consecutive blocks of D/4, sum each
+ *   block in ascending order from +0 with separately rounded multiplies and
+ *   adds, and combine them as ((b0 + b1) + (b2 + b3)); sums over N rows use
+ *   the pairwise tree (adjacent pairs, odd last element carried);
+ *   sign(a) = +1 iff a >= 0.  A sign decision is counted as "fragile" when
+ *   |(float)a| < 1e-6.
+ */
+#ifndef BPC_H
+#define BPC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes (0 = success). */
+#define BPC_OK 0
+#define BPC_EINVAL (-1)       /* null required pointer, bad size or shape */
+#define BPC_EUNSUPPORTED (-2) /* D != 128 or L not in {32, 64, 128} */
+#define BPC_EALIGN (-3)       /* pointer or row stride not 16-byte aligned */
+#define BPC_EWORKSPACE (-4)   /* workspace missing or too small */
+#define BPC_EHIP (-5)         /* a HIP runtime call or launch failed */
+
+/* Static description of a status code. */
+const char* bpc_status_string(int status);
+
+/* Detail of the last failed call on the calling thread ("" if none). */
+const char* bpc_last_error(void);
+
+/* Library version, major * 10000 + minor * 100 + patch. */
+int bpc_version(void);
+
+/*
+ * bpc_build_hash -- binary principal components of each (sequence, KV
+ * head)'s keys (Sec. 3.2, "Binary Principal Components Finding", Algorithm
+ * "Constructing hash codes and corresponding hashing projection"; the
+ * closed-form v for a fixed u is in the Appendix "Procedure Overview").
+ *
+ * For every (b, h) independently, with residual R = K[b,h,0:N,:] and for
+ * i = 0..L-1:
+ *     a_j = R_j . G[i]           (fixed-order fp64 dot, see above)
+ *     u_j = sign(a_j)            code bit i of key j
+ *     v   = (sum_j u_j R_j) / N  (pairwise tree over j, one rounded divide)
+ *     P[i] = (float)v
+ *     R_j = R_j - u_j P[i]       (the stored float P is what is removed)
+ * G [L, D] fp32 holds the random Gaussian directions (v* of the
+ * algorithm), supplied by the caller and shared by all (b, h).
+ *
+ * K         [B, Hkv, >=N, D] bf16, strides sK_b, sK_h, sK_n (elements)
+ * G         [L, D] fp32, contiguous
+ * P_out     [B, Hkv, L, D] fp32, contiguous (written)
+ * codes_out [B, Hkv, >=N, W] uint32, strides sC_b, sC_h (words); key rows
+ *           are W words apart (written)
+ * err_out   [B, Hkv, N] fp32 contiguous, ||k_j - h_j P|| (or NULL)
+ * fragile_out  one device uint64 to which the number of fragile sign
+ *           decisions is ADDED (the caller zeroes it), or NULL
+ * workspace    device memory of at least bpc_build_workspace_bytes(...)
+ *           bytes, 256-byte aligned; its contents on entry do not matter.
+ * Cost: 3 L + 1 kernel launches; the fp64 residual lives in the workspace.
+ */
+size_t bpc_build_workspace_bytes(int B, int Hkv, int N, int D, int L);
+int bpc_build_hash(const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t sK_n,
+                   int B, int Hkv, int N, int D, int L,
+                   const float* G,
+                   float* P_out,
+                   uint32_t* codes_out, int64_t sC_b, int64_t sC_h,
+                   float* err_out,
+                   unsigned long long* fragile_out,
+                   void* workspace, size_t workspace_bytes,
+                   void* stream);
+
+/*
+ * bpc_hash_keys -- hash keys against a given projection (Sec. 3.2,
+ * Algorithm "Given projection, computing hashcode"; also the per-key
+ * "hashing kernel" of the Appendix "CUDA Optimizations on Bitwise
+ * Operations").  Per key: r = k; for i = 0..L-1: u = sign(r . P[i]);
+ * r = r - u P[i]; h_i = u.
+ *
+ * K          [B, Hkv, >=N, D] bf16, strides sK_b, sK_h, sK_n
+ * P          [B, Hkv, L, D] fp32 with strides sP_b, sP_h (elements; rows of
+ *            one head are contiguous).  sP_b = sP_h = 0 shares one P.
+ * codes_out  [B, Hkv, >=N, W] uint32, strides sC_b, sC_h (written)
+ * err_out    [B, Hkv, N] fp32 contiguous ||r_final|| (or NULL)
+ * fragile_out  device uint64 accumulator (or NULL), as above.
+ * No workspace; one kernel launch.
+ */
+int bpc_hash_keys(const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t sK_n,
+                  int B, int Hkv, int N, int D, int L,
+                  const float* P, int64_t sP_b, int64_t sP_h,
+                  uint32_t* codes_out, int64_t sC_b, int64_t sC_h,
+                  float* err_out,
+                  unsigned long long* fragile_out,
+                  void* stream);
+
+/*
+ * bpc_decode_attention -- one decode step of BinaryPC sparse attention
+ * (Sec. 3.2 "Retrieval Phase"; Algorithm "Computing hashing score";
+ * Sec. 4.2 "Kernel Evaluation": search, selection, gathering, attention).
+ *
+ * For every (b, KV head h) with its group of G = Hq / Hkv query heads:
+ *  1. x = sum_g q_g P^T (fixed-order fp64 dots, heads added in ascending
+ *     order); m = max |x_i|; p_i = round-half-away((x_i * 127) / m) in
+ *     [-127, 127] (p = 0 if m = 0).  Packed as 8 planes of W words: plane 0
+ *     bit i = (p_i >= 0), plane 1 + j bit i = bit j of |p_i|.
+ *  2. score of cached key n: c_n = sum_i h_{n,i} p_i, computed as
+ *     sum|p| - 2 * sum_j 2^j popcount(plane_{1+j} & (code_n XOR plane_0)).
+ *  3. the k keys with the largest c (equal scores: lower index first).
+ *  4. out[b, g] = softmax over the selected n of (q_g . K_n) * sm_scale,
+ *     applied to V_n; fp32 accumulation.
+ *
+ * q          [B, Hq, D] bf16, contiguous
+ * K, V       [B, Hkv, >=N, D] bf16, strides (sK_b, sK_h, sK_n) and
+ *            (sV_b, sV_h, sV_n)
+ * codes      [B, Hkv, >=N, W] uint32, strides sC_b, sC_h
+ * P          [B, Hkv, L, D] fp32, strides sP_b, sP_h (0, 0 = shared)
+ * k          1 <= k <= N selected keys per (b, KV head)
+ * out        [B, Hq, D] fp32, contiguous (written)
+ * idx_out    [B, Hkv, k] int32 selected key indices, ascending (or NULL)
+ * score_out  [B, Hkv, N] int32 scores c_n (or NULL)
+ * qcode_out  [B, Hkv, 8, W] uint32 packed query planes (or NULL)
+ * workspace  at least bpc_decode_workspace_bytes(...) bytes, 256-byte
+ *            aligned; contents on entry do not matter.
+ */
+size_t bpc_decode_workspace_bytes(int B, int Hq, int Hkv, int N, int D, int L, int k);
+int bpc_decode_attention(const uint16_t* q,
+                         const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t sK_n,
+                         const uint16_t* V, int64_t sV_b, int64_t sV_h, int64_t sV_n,
+                         const uint32_t* codes, int64_t sC_b, int64_t sC_h,
+                         const float* P, int64_t sP_b, int64_t sP_h,
+                         int B, int Hq, int Hkv, int N, int D, int L, int k,
+                         float sm_scale,
+                         float* out,
+                         int32_t* idx_out,
+                         int32_t* score_out,
+                         uint32_t* qcode_out,
+                         void* workspace, size_t workspace_bytes,
+                         void* stream);
+
+/*
+ * bpc_decode_attention_profiled -- bpc_decode_attention that also records
+ * caller-created hipEvent_t handles on `stream` at the stage boundaries
+ * (query packing | scoring | threshold | selection | attention | merge):
+ * events[0] before the first stage and events[s + 1] after stage s, so
+ * n_events must be BPC_DECODE_STAGES + 1.  For measuring only.
+ */
+#define BPC_DECODE_STAGES 6
+int bpc_decode_attention_profiled(const uint16_t* q,
+                                  const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t sK_n,
+                                  const uint16_t* V, int64_t sV_b, int64_t sV_h, int64_t sV_n,
+                                  const uint32_t* codes, int64_t sC_b, int64_t sC_h,
+                                  const float* P, int64_t sP_b, int64_t sP_h,
+                                  int B, int Hq, int Hkv, int N, int D, int L, int k,
+                                  float sm_scale,
+                                  float* out,
+                                  int32_t* idx_out,
+                                  int32_t* score_out,
+                                  uint32_t* qcode_out,
+                                  void* workspace, size_t workspace_bytes,
+                                  void* stream,
+                                  void* const* events, int n_events);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BPC_H */

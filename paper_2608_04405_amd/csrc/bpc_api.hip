@@ -1,0 +1,278 @@
+// Host side of the C ABI: argument checks, workspace layouts, dispatch.
+//
+// Every check runs before anything is enqueued, so a call that returns an
+// error has launched nothing and written no output.
+
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "bpc_internal.h"
+
+namespace bpc {
+
+static thread_local char g_last_error[512] = "";
+
+static int fail(int status, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+  va_end(ap);
+  return status;
+}
+
+static int hip_fail(hipError_t e, const char* what) {
+  return fail(BPC_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+static size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+static bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+static int check_code_len(int L) {
+  if (L != 32 && L != 64 && L != 128) return fail(BPC_EUNSUPPORTED, "L=%d: code length must be 32, 64 or 128", L);
+  return BPC_OK;
+}
+
+static int check_head_dim(int D) {
+  if (D != kHeadDim) return fail(BPC_EUNSUPPORTED, "D=%d: only head_dim 128 is supported", D);
+  return BPC_OK;
+}
+
+// A bf16 [B, H, >=N, D] tensor given by strides.
+static int check_kv(const char* name, const uint16_t* p, int64_t sb, int64_t sh, int64_t sn) {
+  if (!p) return fail(BPC_EINVAL, "%s is NULL", name);
+  if (sb < 0 || sh < 0 || sn < kHeadDim)
+    return fail(BPC_EINVAL, "%s strides (%lld, %lld, %lld) invalid: need s_b, s_h >= 0 and s_n >= 128", name,
+                (long long)sb, (long long)sh, (long long)sn);
+  if (!aligned16(p) || (sb % 8) || (sh % 8) || (sn % 8))
+    return fail(BPC_EALIGN, "%s must be 16-byte aligned with strides multiple of 8 elements", name);
+  return BPC_OK;
+}
+
+static int check_codes(const char* name, const void* p, int64_t sb, int64_t sh, int W) {
+  if (!p) return fail(BPC_EINVAL, "%s is NULL", name);
+  if (sb < 0 || sh < 0) return fail(BPC_EINVAL, "%s strides must be >= 0", name);
+  if (!aligned16(p) || (sb % W) || (sh % W))
+    return fail(BPC_EALIGN, "%s must be 16-byte aligned with strides multiple of W=%d words", name, W);
+  return BPC_OK;
+}
+
+static int check_proj(const float* P, int64_t sb, int64_t sh) {
+  if (!P) return fail(BPC_EINVAL, "P is NULL");
+  if (sb < 0 || sh < 0) return fail(BPC_EINVAL, "P strides must be >= 0");
+  if (!aligned16(P) || (sb % 4) || (sh % 4))
+    return fail(BPC_EALIGN, "P must be 16-byte aligned with strides multiple of 4 floats");
+  return BPC_OK;
+}
+
+static int check_opt_aligned(const char* name, const void* p) {
+  if (p && !aligned16(p)) return fail(BPC_EALIGN, "%s must be 16-byte aligned", name);
+  return BPC_OK;
+}
+
+DecodeLayout decode_layout(int B, int Hq, int Hkv, int N, int L, int k) {
+  DecodeLayout d{};
+  const size_t BH = (size_t)B * Hkv;
+  d.W = L / 32;
+  d.G = Hq / Hkv;
+  d.nslices = (N + kSlice - 1) / kSlice;
+  d.nchunks = (k + kAttnChunk - 1) / kAttnChunk;
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    size_t at = o;
+    o = align_up(o + bytes, 256);
+    return at;
+  };
+  d.off_qcode = take(BH * 8 * d.W * sizeof(uint32_t));
+  d.off_T = take(BH * sizeof(int32_t));
+  d.off_cand = take(BH * d.nslices * (size_t)kSlice * sizeof(uint32_t));
+  d.off_cand_count = take(BH * d.nslices * sizeof(int32_t));
+  d.off_hist_fine = take(BH * d.nslices * (size_t)fine_stride(L) * sizeof(uint16_t));
+  d.off_hist_coarse = take(BH * d.nslices * (size_t)kCoarseBins * sizeof(uint32_t));
+  d.off_sel_info = take(BH * 4 * sizeof(int32_t));
+  d.off_sel_base = take(BH * d.nslices * sizeof(int32_t));
+  d.off_tie_base = take(BH * d.nslices * sizeof(int32_t));
+  d.off_idx = take(BH * (size_t)k * sizeof(int32_t));
+  d.off_part = take(BH * d.nchunks * (size_t)d.G * (kHeadDim + 2) * sizeof(float));
+  d.total = o;
+  return d;
+}
+
+BuildLayout build_layout(int B, int Hkv, int N, int L) {
+  (void)L;
+  BuildLayout b{};
+  const size_t BH = (size_t)B * Hkv;
+  b.nchunks = (N + kBuildRows - 1) / kBuildRows;
+  size_t o = 0;
+  b.off_R = o;
+  o = align_up(o + BH * kHeadDim * (size_t)N * sizeof(double), 256);
+  b.off_part = o;
+  o = align_up(o + BH * b.nchunks * (size_t)kHeadDim * sizeof(double), 256);
+  b.total = o;
+  return b;
+}
+
+static int check_sizes(int B, int Hkv, int N) {
+  if (B < 1 || Hkv < 1 || N < 1) return fail(BPC_EINVAL, "B=%d, Hkv=%d, N=%d must all be >= 1", B, Hkv, N);
+  if ((int64_t)N > (int64_t)(1 << 30)) return fail(BPC_EINVAL, "N=%d too large", N);
+  return BPC_OK;
+}
+
+}  // namespace bpc
+
+using namespace bpc;
+
+extern "C" {
+
+const char* bpc_status_string(int status) {
+  switch (status) {
+    case BPC_OK: return "ok";
+    case BPC_EINVAL: return "invalid argument";
+    case BPC_EUNSUPPORTED: return "unsupported shape";
+    case BPC_EALIGN: return "misaligned pointer or stride";
+    case BPC_EWORKSPACE: return "workspace missing or too small";
+    case BPC_EHIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+const char* bpc_last_error(void) { return g_last_error; }
+
+int bpc_version(void) { return 100; }
+
+size_t bpc_build_workspace_bytes(int B, int Hkv, int N, int D, int L) {
+  if (B < 1 || Hkv < 1 || N < 1 || D != kHeadDim) return 0;
+  return build_layout(B, Hkv, N, L).total;
+}
+
+int bpc_build_hash(const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t sK_n, int B, int Hkv, int N,
+                   int D, int L, const float* G, float* P_out, uint32_t* codes_out, int64_t sC_b,
+                   int64_t sC_h, float* err_out, unsigned long long* fragile_out, void* workspace,
+                   size_t workspace_bytes, void* stream) {
+  g_last_error[0] = 0;
+  int st;
+  if ((st = check_sizes(B, Hkv, N))) return st;
+  if ((st = check_head_dim(D))) return st;
+  if ((st = check_code_len(L))) return st;
+  if ((st = check_kv("K", K, sK_b, sK_h, sK_n))) return st;
+  if (!G || !P_out) return fail(BPC_EINVAL, "G and P_out are required");
+  if (!aligned16(G) || !aligned16(P_out)) return fail(BPC_EALIGN, "G and P_out must be 16-byte aligned");
+  if ((st = check_codes("codes_out", codes_out, sC_b, sC_h, L / 32))) return st;
+  if ((st = check_opt_aligned("err_out", err_out))) return st;
+  const BuildLayout lay = build_layout(B, Hkv, N, L);
+  if (!workspace || workspace_bytes < lay.total)
+    return fail(BPC_EWORKSPACE, "workspace of %zu bytes given, %zu needed", workspace ? workspace_bytes : 0,
+                lay.total);
+  if (reinterpret_cast<uintptr_t>(workspace) & 255u) return fail(BPC_EALIGN, "workspace must be 256-byte aligned");
+  hipError_t e = launch_build(K, sK_b, sK_h, sK_n, B, Hkv, N, L, G, P_out, codes_out, sC_b, sC_h, err_out,
+                              fragile_out, static_cast<char*>(workspace), static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "bpc_build_hash launch");
+  return BPC_OK;
+}
+
+int bpc_hash_keys(const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t sK_n, int B, int Hkv, int N, int D,
+                  int L, const float* P, int64_t sP_b, int64_t sP_h, uint32_t* codes_out, int64_t sC_b,
+                  int64_t sC_h, float* err_out, unsigned long long* fragile_out, void* stream) {
+  g_last_error[0] = 0;
+  int st;
+  if ((st = check_sizes(B, Hkv, N))) return st;
+  if ((st = check_head_dim(D))) return st;
+  if ((st = check_code_len(L))) return st;
+  if ((st = check_kv("K", K, sK_b, sK_h, sK_n))) return st;
+  if ((st = check_proj(P, sP_b, sP_h))) return st;
+  if ((st = check_codes("codes_out", codes_out, sC_b, sC_h, L / 32))) return st;
+  if ((st = check_opt_aligned("err_out", err_out))) return st;
+  hipError_t e = launch_hash(K, sK_b, sK_h, sK_n, B, Hkv, N, L, P, sP_b, sP_h, codes_out, sC_b, sC_h, err_out,
+                             fragile_out, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "bpc_hash_keys launch");
+  return BPC_OK;
+}
+
+size_t bpc_decode_workspace_bytes(int B, int Hq, int Hkv, int N, int D, int L, int k) {
+  if (B < 1 || Hkv < 1 || Hq < Hkv || Hq % Hkv || N < 1 || k < 1 || k > N || D != kHeadDim) return 0;
+  if (L != 32 && L != 64 && L != 128) return 0;
+  return decode_layout(B, Hq, Hkv, N, L, k).total;
+}
+
+static int decode_impl(const uint16_t* q, const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t sK_n,
+                       const uint16_t* V, int64_t sV_b, int64_t sV_h, int64_t sV_n, const uint32_t* codes,
+                       int64_t sC_b, int64_t sC_h, const float* P, int64_t sP_b, int64_t sP_h, int B, int Hq,
+                       int Hkv, int N, int D, int L, int k, float sm_scale, float* out, int32_t* idx_out,
+                       int32_t* score_out, uint32_t* qcode_out, void* workspace, size_t workspace_bytes,
+                       void* stream, void* const* events, int n_events) {
+  g_last_error[0] = 0;
+  int st;
+  if ((st = check_sizes(B, Hkv, N))) return st;
+  if (Hq < Hkv || Hq % Hkv) return fail(BPC_EINVAL, "Hq=%d must be a positive multiple of Hkv=%d", Hq, Hkv);
+  {
+    const int G = Hq / Hkv;
+    if (G > kMaxGroup || (G & (G - 1)))
+      return fail(BPC_EUNSUPPORTED, "group size Hq/Hkv=%d must be 1, 2, 4, 8 or 16", G);
+  }
+  if ((st = check_head_dim(D))) return st;
+  if ((st = check_code_len(L))) return st;
+  if (k < 1 || k > N) return fail(BPC_EINVAL, "k=%d must satisfy 1 <= k <= N=%d", k, N);
+  if (!(sm_scale > 0.0f) || !__builtin_isfinite(sm_scale))
+    return fail(BPC_EINVAL, "sm_scale must be finite and > 0");
+  if (!q || !out) return fail(BPC_EINVAL, "q and out are required");
+  if (!aligned16(q) || !aligned16(out)) return fail(BPC_EALIGN, "q and out must be 16-byte aligned");
+  if ((st = check_kv("K", K, sK_b, sK_h, sK_n))) return st;
+  if ((st = check_kv("V", V, sV_b, sV_h, sV_n))) return st;
+  if ((st = check_codes("codes", codes, sC_b, sC_h, L / 32))) return st;
+  if ((st = check_proj(P, sP_b, sP_h))) return st;
+  if ((st = check_opt_aligned("idx_out", idx_out))) return st;
+  if ((st = check_opt_aligned("score_out", score_out))) return st;
+  if ((st = check_opt_aligned("qcode_out", qcode_out))) return st;
+  if (events && n_events != BPC_DECODE_STAGES + 1)
+    return fail(BPC_EINVAL, "n_events=%d, expected %d", n_events, BPC_DECODE_STAGES + 1);
+  const DecodeLayout lay = decode_layout(B, Hq, Hkv, N, L, k);
+  if (!workspace || workspace_bytes < lay.total)
+    return fail(BPC_EWORKSPACE, "workspace of %zu bytes given, %zu needed", workspace ? workspace_bytes : 0,
+                lay.total);
+  if (reinterpret_cast<uintptr_t>(workspace) & 255u) return fail(BPC_EALIGN, "workspace must be 256-byte aligned");
+
+  DecodeArgs a{};
+  a.q = q;
+  a.K = K, a.sK_b = sK_b, a.sK_h = sK_h, a.sK_n = sK_n;
+  a.V = V, a.sV_b = sV_b, a.sV_h = sV_h, a.sV_n = sV_n;
+  a.codes = codes, a.sC_b = sC_b, a.sC_h = sC_h;
+  a.P = P, a.sP_b = sP_b, a.sP_h = sP_h;
+  a.B = B, a.Hq = Hq, a.Hkv = Hkv, a.N = N, a.L = L, a.k = k;
+  a.sm_scale = sm_scale;
+  a.out = out, a.idx_out = idx_out, a.score_out = score_out, a.qcode_out = qcode_out;
+  a.ws = static_cast<char*>(workspace);
+  a.stream = static_cast<hipStream_t>(stream);
+  a.events = reinterpret_cast<hipEvent_t const*>(events);
+  hipError_t e = launch_decode(a);
+  if (e != hipSuccess) return hip_fail(e, "bpc_decode_attention launch");
+  return BPC_OK;
+}
+
+int bpc_decode_attention(const uint16_t* q, const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t sK_n,
+                         const uint16_t* V, int64_t sV_b, int64_t sV_h, int64_t sV_n, const uint32_t* codes,
+                         int64_t sC_b, int64_t sC_h, const float* P, int64_t sP_b, int64_t sP_h, int B, int Hq,
+                         int Hkv, int N, int D, int L, int k, float sm_scale, float* out, int32_t* idx_out,
+                         int32_t* score_out, uint32_t* qcode_out, void* workspace, size_t workspace_bytes,
+                         void* stream) {
+  return decode_impl(q, K, sK_b, sK_h, sK_n, V, sV_b, sV_h, sV_n, codes, sC_b, sC_h, P, sP_b, sP_h, B, Hq, Hkv,
+                     N, D, L, k, sm_scale, out, idx_out, score_out, qcode_out, workspace, workspace_bytes, stream,
+                     nullptr, 0);
+}
+
+int bpc_decode_attention_profiled(const uint16_t* q, const uint16_t* K, int64_t sK_b, int64_t sK_h,
+                                  int64_t sK_n, const uint16_t* V, int64_t sV_b, int64_t sV_h, int64_t sV_n,
+                                  const uint32_t* codes, int64_t sC_b, int64_t sC_h, const float* P,
+                                  int64_t sP_b, int64_t sP_h, int B, int Hq, int Hkv, int N, int D, int L, int k,
+                                  float sm_scale, float* out, int32_t* idx_out, int32_t* score_out,
+                                  uint32_t* qcode_out, void* workspace, size_t workspace_bytes, void* stream,
+                                  void* const* events, int n_events) {
+  if (!events) return fail(BPC_EINVAL, "events is NULL");
+  for (int i = 0; i < n_events; ++i)
+    if (!events[i]) return fail(BPC_EINVAL, "events[%d] is NULL", i);
+  return decode_impl(q, K, sK_b, sK_h, sK_n, V, sV_b, sV_h, sV_n, codes, sC_b, sC_h, P, sP_b, sP_h, B, Hq, Hkv,
+                     N, D, L, k, sm_scale, out, idx_out, score_out, qcode_out, workspace, workspace_bytes, stream,
+                     events, n_events);
+}
+
+}  // extern "C"

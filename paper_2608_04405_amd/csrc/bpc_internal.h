@@ -1,0 +1,99 @@
+// Internal declarations shared by the HIP translation units of libbpc.
+//
+// Every file of the library is compiled with -ffp-contract=off: the
+// sign-deciding sums must round after each multiply and each add, exactly
+// as the fixed-order arithmetic documented in include/bpc.h prescribes.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/bpc.h"
+
+namespace bpc {
+
+constexpr int kHeadDim = 128;
+
+// ---- decode tiling ---------------------------------------------------------
+// One scoring workgroup owns a slice of kSlice consecutive keys of one
+// (sequence, KV head); the slice's distances stay in LDS.
+constexpr int kSlice = 16384;
+constexpr int kScanThreads = 1024;
+// Selected keys attended by one attention workgroup.
+constexpr int kAttnChunk = 256;
+constexpr int kAttnThreads = 256;
+constexpr int kCoarseShift = 7;  // coarse histogram bin = distance >> 7
+constexpr int kCoarseBins = 128;
+constexpr int kMaxGroup = 16;  // query heads per KV head
+
+// Weighted Hamming distances lie in [0, 127 L].
+__host__ __device__ constexpr int dist_bins(int L) { return 127 * L + 1; }
+// Per-slice fine-histogram stride (u16 counts), padded to 16 bytes.
+__host__ __device__ constexpr int fine_stride(int L) { return (dist_bins(L) + 7) & ~7; }
+
+// ---- build tiling ----------------------------------------------------------
+constexpr int kBuildRows = 256;  // rows per workgroup in the build passes
+
+// ---- workspace layouts -----------------------------------------------------
+struct DecodeLayout {
+  int nslices, nchunks, G, W;
+  size_t off_qcode, off_T, off_cand, off_cand_count, off_hist_fine, off_hist_coarse,
+      off_sel_info, off_sel_base, off_tie_base, off_idx, off_part, total;
+};
+
+struct BuildLayout {
+  int nchunks;
+  size_t off_R, off_part, total;
+};
+
+DecodeLayout decode_layout(int B, int Hq, int Hkv, int N, int L, int k);
+BuildLayout build_layout(int B, int Hkv, int N, int L);
+
+// ---- launchers (enqueue only; arguments already validated) ---------------
+struct DecodeArgs {
+  const uint16_t* q;
+  const uint16_t* K;
+  int64_t sK_b, sK_h, sK_n;
+  const uint16_t* V;
+  int64_t sV_b, sV_h, sV_n;
+  const uint32_t* codes;
+  int64_t sC_b, sC_h;
+  const float* P;
+  int64_t sP_b, sP_h;
+  int B, Hq, Hkv, N, L, k;
+  float sm_scale;
+  float* out;
+  int32_t* idx_out;
+  int32_t* score_out;
+  uint32_t* qcode_out;
+  char* ws;
+  hipStream_t stream;
+  hipEvent_t const* events;  // BPC_DECODE_STAGES + 1 handles, or nullptr
+};
+
+hipError_t launch_decode(const DecodeArgs& a);
+
+hipError_t launch_hash(const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t sK_n, int B, int Hkv,
+                       int N, int L, const float* P, int64_t sP_b, int64_t sP_h, uint32_t* codes,
+                       int64_t sC_b, int64_t sC_h, float* err, unsigned long long* fragile,
+                       hipStream_t stream);
+
+hipError_t launch_build(const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t sK_n, int B, int Hkv,
+                        int N, int L, const float* G, float* P, uint32_t* codes, int64_t sC_b,
+                        int64_t sC_h, float* err, unsigned long long* fragile, char* ws,
+                        hipStream_t stream);
+
+// ---- device helpers ----------------------------------------------------------
+__device__ __forceinline__ double bf16_to_f64(uint16_t b) {
+  return (double)__uint_as_float(((uint32_t)b) << 16);
+}
+__device__ __forceinline__ float bf16_to_f32(uint32_t b) { return __uint_as_float(b << 16); }
+
+// Rounded fp64 add and multiply; the file-wide -ffp-contract=off keeps them
+// from being fused.
+__device__ __forceinline__ double dadd(double a, double b) { return a + b; }
+__device__ __forceinline__ double dmul(double a, double b) { return a * b; }
+
+__device__ __forceinline__ bool fragile_decision(double a) { return fabsf((float)a) < 1e-6f; }
+
+}  // namespace bpc

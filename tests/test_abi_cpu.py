@@ -1,0 +1,161 @@
+"""The C ABI on the CPU: the library loads, exports what include/bpc.h
+declares, sizes its workspaces, and rejects bad arguments on the host.
+
+Every call here fails argument checking by construction (the pointers are
+fake), so nothing is ever enqueued on a device.
+"""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "bpc.h")
+LIB = os.path.join(ROOT, "paper_2608_04405_amd", "libbpc.so")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(LIB), reason="libbpc.so not built")
+
+OK, EINVAL, EUNSUP, EALIGN, EWS, EHIP = 0, -1, -2, -3, -4, -5
+FAKE = 0x10000  # 16-byte aligned, never dereferenced: every call below fails validation first
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(bpc_[a-z_]+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    L = ctypes.CDLL(LIB)
+    L.bpc_status_string.restype = ctypes.c_char_p
+    L.bpc_last_error.restype = ctypes.c_char_p
+    L.bpc_decode_workspace_bytes.restype = ctypes.c_size_t
+    L.bpc_build_workspace_bytes.restype = ctypes.c_size_t
+    return L
+
+
+def test_exports_every_declared_symbol(lib):
+    names = declared_functions()
+    assert {"bpc_build_hash", "bpc_hash_keys", "bpc_decode_attention"} <= set(names)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_status_strings(lib):
+    for code, word in ((OK, b"ok"), (EINVAL, b"invalid"), (EUNSUP, b"unsupported"), (EALIGN, b"misaligned"),
+                       (EWS, b"workspace"), (EHIP, b"HIP")):
+        assert word in lib.bpc_status_string(code)
+    assert lib.bpc_version() >= 100
+
+
+def test_workspace_sizes(lib):
+    ws = lib.bpc_decode_workspace_bytes
+    assert ws(16, 32, 8, 131072, 128, 64, 2622) > 0
+    assert ws(16, 32, 8, 131072, 128, 64, 2622) % 256 == 0
+    assert ws(1, 8, 8, 4096, 128, 32, 82) < ws(1, 8, 8, 40000, 128, 32, 82)
+    assert ws(1, 8, 8, 4096, 64, 32, 82) == 0  # D != 128
+    assert ws(1, 8, 8, 4096, 128, 48, 82) == 0  # bad L
+    assert ws(1, 8, 8, 4096, 128, 32, 0) == 0  # k < 1
+    assert ws(1, 8, 8, 4096, 128, 32, 4097) == 0  # k > N
+    assert ws(1, 6, 4, 4096, 128, 32, 8) == 0  # Hq % Hkv
+    b = lib.bpc_build_workspace_bytes(2, 8, 1000, 128, 64)
+    assert b >= 2 * 8 * 1000 * 128 * 8  # the fp64 residual
+
+
+_i64 = ctypes.c_int64
+
+
+def _decode(lib, **kw):
+    a = dict(q=FAKE, K=FAKE, sKb=8 * 4096 * 128, sKh=4096 * 128, sKn=128, V=FAKE, sVb=8 * 4096 * 128,
+             sVh=4096 * 128, sVn=128, codes=FAKE, sCb=8 * 4096, sCh=4096, P=FAKE, sPb=8 * 32 * 128, sPh=32 * 128,
+             B=1, Hq=8, Hkv=8, N=4096, D=128, L=32, k=82, sm=0.088, out=FAKE, idx=None, score=None, qcode=None,
+             ws=FAKE, ws_bytes=0, stream=None)
+    a.update(kw)
+    f = lib.bpc_decode_attention
+    f.restype = ctypes.c_int
+    return f(ctypes.c_void_p(a["q"]), ctypes.c_void_p(a["K"]), _i64(a["sKb"]), _i64(a["sKh"]), _i64(a["sKn"]),
+             ctypes.c_void_p(a["V"]), _i64(a["sVb"]), _i64(a["sVh"]), _i64(a["sVn"]), ctypes.c_void_p(a["codes"]),
+             _i64(a["sCb"]), _i64(a["sCh"]), ctypes.c_void_p(a["P"]), _i64(a["sPb"]), _i64(a["sPh"]), a["B"],
+             a["Hq"], a["Hkv"], a["N"], a["D"], a["L"], a["k"], ctypes.c_float(a["sm"]), ctypes.c_void_p(a["out"]),
+             ctypes.c_void_p(a["idx"]), ctypes.c_void_p(a["score"]), ctypes.c_void_p(a["qcode"]),
+             ctypes.c_void_p(a["ws"]), ctypes.c_size_t(a["ws_bytes"]), ctypes.c_void_p(a["stream"]))
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(q=None), EINVAL),
+    (dict(out=None), EINVAL),
+    (dict(K=None), EINVAL),
+    (dict(codes=None), EINVAL),
+    (dict(P=None), EINVAL),
+    (dict(B=0), EINVAL),
+    (dict(N=0), EINVAL),
+    (dict(Hq=12), EINVAL),          # not a multiple of Hkv
+    (dict(Hq=24), EUNSUP),          # group of 3
+    (dict(Hq=8 * 32), EUNSUP),      # group of 32
+    (dict(k=0), EINVAL),
+    (dict(k=4097), EINVAL),
+    (dict(D=64), EUNSUP),
+    (dict(L=48), EUNSUP),
+    (dict(sm=0.0), EINVAL),
+    (dict(sm=float("nan")), EINVAL),
+    (dict(sKn=100), EINVAL),
+    (dict(sKn=132), EALIGN),
+    (dict(K=FAKE + 8), EALIGN),
+    (dict(q=FAKE + 2), EALIGN),
+    (dict(idx=FAKE + 4), EALIGN),
+    (dict(sPh=32 * 128 + 2), EALIGN),
+    (dict(ws=None), EWS),
+    (dict(ws_bytes=1024), EWS),     # too small
+])
+def test_decode_rejects(lib, kw, code):
+    assert _decode(lib, **kw) == code
+    assert lib.bpc_last_error() != b""
+
+
+def test_decode_rejects_misaligned_workspace(lib):
+    need = lib.bpc_decode_workspace_bytes(1, 8, 8, 4096, 128, 32, 82)
+    assert _decode(lib, ws=FAKE + 16, ws_bytes=need) == EALIGN
+
+
+def _hash(lib, **kw):
+    a = dict(K=FAKE, sKb=0, sKh=4096 * 128, sKn=128, B=1, Hkv=8, N=4096, D=128, L=64, P=FAKE, sPb=0, sPh=0,
+             codes=FAKE, sCb=8 * 4096 * 2, sCh=4096 * 2, err=None, frag=None, stream=None)
+    a.update(kw)
+    f = lib.bpc_hash_keys
+    f.restype = ctypes.c_int
+    return f(ctypes.c_void_p(a["K"]), _i64(a["sKb"]), _i64(a["sKh"]), _i64(a["sKn"]), a["B"], a["Hkv"], a["N"],
+             a["D"], a["L"], ctypes.c_void_p(a["P"]), _i64(a["sPb"]), _i64(a["sPh"]), ctypes.c_void_p(a["codes"]),
+             _i64(a["sCb"]), _i64(a["sCh"]), ctypes.c_void_p(a["err"]), ctypes.c_void_p(a["frag"]),
+             ctypes.c_void_p(a["stream"]))
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(K=None), EINVAL), (dict(P=None), EINVAL), (dict(codes=None), EINVAL), (dict(N=-1), EINVAL),
+    (dict(L=96), EUNSUP), (dict(D=256), EUNSUP), (dict(sCh=4096 * 2 + 1), EALIGN), (dict(P=FAKE + 4), EALIGN),
+    (dict(err=FAKE + 4), EALIGN), (dict(sPb=-4), EINVAL),
+])
+def test_hash_rejects(lib, kw, code):
+    assert _hash(lib, **kw) == code
+
+
+def _build(lib, **kw):
+    a = dict(K=FAKE, sKb=0, sKh=4096 * 128, sKn=128, B=1, Hkv=8, N=4096, D=128, L=32, G=FAKE, P=FAKE,
+             codes=FAKE, sCb=8 * 4096, sCh=4096, err=None, frag=None, ws=FAKE, ws_bytes=0, stream=None)
+    a.update(kw)
+    f = lib.bpc_build_hash
+    f.restype = ctypes.c_int
+    return f(ctypes.c_void_p(a["K"]), _i64(a["sKb"]), _i64(a["sKh"]), _i64(a["sKn"]), a["B"], a["Hkv"], a["N"],
+             a["D"], a["L"], ctypes.c_void_p(a["G"]), ctypes.c_void_p(a["P"]), ctypes.c_void_p(a["codes"]),
+             _i64(a["sCb"]), _i64(a["sCh"]), ctypes.c_void_p(a["err"]), ctypes.c_void_p(a["frag"]),
+             ctypes.c_void_p(a["ws"]), ctypes.c_size_t(a["ws_bytes"]), ctypes.c_void_p(a["stream"]))
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(G=None), EINVAL), (dict(P=None), EINVAL), (dict(codes=None), EINVAL), (dict(L=16), EUNSUP),
+    (dict(ws=None), EWS), (dict(ws_bytes=100), EWS), (dict(G=FAKE + 8), EALIGN),
+])
+def test_build_rejects(lib, kw, code):
+    assert _build(lib, **kw) == code
