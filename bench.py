@@ -1,0 +1,258 @@
+"""Benchmark of the BinaryPC decode hot path on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W]
+
+Workload: batch 16, 32 query / 8 KV heads, head_dim 128, 131072 cached keys
+per sequence (bf16 K/V), 64-bit codes, 2 % budget (k = 2622 per KV head).
+A step is one full decode step (query packing, XOR/popcount scan of every
+cached code, exact top-k, gathered sparse attention, merge) for the whole
+batch.  Four independent instances of the workload (different seeds) are
+used in turn so that consecutive steps do not re-read each other's data from
+the 256 MB last-level cache; all inputs are resident in HBM before timing.
+
+Prints one JSON line with the metric (decode keys/s = B * Hkv * N / step
+time), the stage breakdown, the roofline of the dominant kernel, the
+prefill (binary-PC build and key hashing) timings and the CPU oracle's
+throughput on a bounded sample.
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "decode attention keys/sec/GPU at 128K ctx (hash+top-k+sparse attn); % HBM peak"
+HBM_PEAK_GBS = 8000.0
+PMC_FILE = os.path.join(ROOT, "profiles", "pmc_decode_batch16_128k.json")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_04405_amd", "csrc", f)
+                  for f in ("decode_kernels.hip", "bpc_internal.h")]
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=30)
+    ap.add_argument("--instances", type=int, default=4)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-prefill", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="also run a plain 1 GiB device copy (counter calibration for rocprofv3 --pmc)")
+    ap.add_argument("--cpu-sample-heads", type=int, default=64)
+    return ap.parse_args()
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def source_sha() -> str:
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        h.update(open(p, "rb").read())
+    return h.hexdigest()[:16]
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path (the decode step of every "
+              "(sequence, KV head) is independent; see DESIGN.md for how it would shard).", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2608_04405_amd as bpc
+    from workloads import config_by_name, make_layer
+
+    cfg = config_by_name("batch16_128k")
+    dev = torch.device("cuda:0")
+    B, Hq, Hkv, D, N, L, k = cfg.B, cfg.Hq, cfg.Hkv, cfg.D, cfg.N, cfg.L, cfg.k
+    sm = 1.0 / math.sqrt(D)
+    W = L // 32
+
+    # ---------------------------------------------------------------- inputs
+    insts = []
+    t0 = time.time()
+    for i in range(args.instances):
+        d = make_layer(cfg, layer=i, device=dev)
+        insts.append({"q": d["q"], "K": d["K"], "V": d["V"], "G": d["G"].to(dev)})
+        del d
+    torch.cuda.synchronize()
+    log(f"generated {args.instances} instances in {time.time() - t0:.1f}s")
+
+    # ---------------------------------------------------------------- prefill
+    ws_build = torch.empty(bpc.build_workspace_bytes(B, Hkv, N, L), dtype=torch.uint8, device=dev)
+    prefill = {}
+    for i, it in enumerate(insts):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        ev[0].record()
+        P, codes, _ = bpc.build_hash(it["K"], it["G"], workspace=ws_build)
+        ev[1].record()
+        if i == 0 and not args.no_prefill:
+            codes2, _ = bpc.hash_keys(it["K"], P)
+        ev[2].record()
+        torch.cuda.synchronize()
+        it["P"], it["codes"] = P, codes
+        if i == 0 and not args.no_prefill:
+            build_ms = ev[0].elapsed_time(ev[1])
+            hash_ms = ev[1].elapsed_time(ev[2])
+            keys = B * Hkv * N
+            prefill = {"build_ms": round(build_ms, 3), "hash_ms": round(hash_ms, 3),
+                       "build_keys_per_s": keys / (build_ms / 1e3), "hash_keys_per_s": keys / (hash_ms / 1e3),
+                       "what": "Algorithm 1 (build P and codes) and Algorithm 2 (hash every key) for the whole "
+                               "batch, fp64 fixed-order arithmetic"}
+            del codes2
+    del ws_build
+    torch.cuda.empty_cache()
+    log(f"prefill {prefill}")
+
+    ws = torch.empty(bpc.decode_workspace_bytes(B, Hq, Hkv, N, L, k), dtype=torch.uint8, device=dev)
+    outs = [torch.empty(B, Hq, D, dtype=torch.float32, device=dev) for _ in insts]
+
+    def step(j, events=None):
+        it = insts[j % len(insts)]
+        bpc.decode_attention(it["q"], it["K"], it["V"], it["codes"], it["P"], k, sm, out=outs[j % len(insts)],
+                             workspace=ws, events=events)
+
+    if args.copy_probe:
+        src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
+    # ---------------------------------------------------------------- timed region
+    for j in range(args.warmup):
+        step(j)
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    wall0 = time.perf_counter()
+    start.record()
+    for j in range(args.steps):
+        step(j)
+    end.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    ms_per_step = start.elapsed_time(end) / args.steps
+    keys_per_step = B * Hkv * N
+    value = keys_per_step / (ms_per_step / 1e3)
+    log(f"{ms_per_step * 1e3:.1f} us/step, {value:.4g} keys/s (wall {wall:.3f}s)")
+
+    # ---------------------------------------------------------------- stage breakdown (same steps, with events)
+    nst = bpc.DECODE_STAGES
+    stage_ms = np.zeros(nst)
+    prof_steps = max(10, min(args.steps, 100))
+    evsets = [[torch.cuda.Event(enable_timing=True) for _ in range(nst + 1)] for _ in range(prof_steps)]
+    for j in range(prof_steps):
+        step(j, events=evsets[j])
+    torch.cuda.synchronize()
+    for evs in evsets:
+        for s in range(nst):
+            stage_ms[s] += evs[s].elapsed_time(evs[s + 1])
+    stage_ms /= prof_steps
+    stages = {n: round(float(t) * 1e3, 2) for n, t in zip(bpc.DECODE_STAGE_NAMES, stage_ms)}  # microseconds
+    log(f"stages (us): {stages}")
+
+    # algorithmic bytes (per step): codes read, gathered K+V rows, P, q and out
+    BH = B * Hkv
+    code_bytes = BH * N * W * 4
+    gather_bytes = BH * k * 2 * D * 2
+    p_bytes = BH * L * D * 4
+    qo_bytes = B * Hq * D * (2 + 4)
+    step_bytes = code_bytes + gather_bytes + p_bytes + qo_bytes
+    per_kernel_bytes = {"scan": code_bytes, "attend": gather_bytes + B * Hq * D * 2,
+                        "qpack": p_bytes + B * Hq * D * 2}
+    # dominant kernel: the stage with the largest time among the HBM streamers
+    dom = max(("scan", "attend"), key=lambda n: stages[n])
+    dom_us = stages[dom]
+    achieved = per_kernel_bytes[dom] / (dom_us * 1e-6) / 1e9
+    traffic = None
+    if os.path.exists(PMC_FILE):
+        pmc = json.load(open(PMC_FILE))
+        if pmc.get("source_sha") == source_sha() and dom in pmc.get("kernels", {}):
+            traffic = pmc["kernels"][dom]["hbm_bytes_per_launch"]
+    roofline = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+                "algorithmic_bytes_per_launch": per_kernel_bytes[dom], "avg_launch_us": dom_us}
+    step_gbs = step_bytes / (ms_per_step * 1e-3) / 1e9
+
+    # ---------------------------------------------------------------- CPU oracle baseline
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(cfg, insts[0], args.cpu_sample_heads)
+
+    line = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "keys/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u32+f32",
+        "data": "synthetic",
+        "config": {"workload": cfg.name, "B": B, "Hq": Hq, "Hkv": Hkv, "head_dim": D, "N": N, "code_bits": L,
+                   "k": k, "budget": "2%", "instances": args.instances},
+        "hbm_frac_step": round(step_gbs / HBM_PEAK_GBS, 4),
+        "step_algorithmic_bytes": step_bytes,
+        "step_GBps": round(step_gbs, 1),
+        "stages_us": stages,
+        "roofline": roofline,
+        "prefill": prefill,
+        "cpu_baseline": cpu,
+        "wall_s_timed": round(wall, 4),
+    }
+    print(json.dumps(line), flush=True)
+
+
+def cpu_baseline(cfg, inst, heads: int):
+    """The oracle's decode step, timed on host cores for `heads` (b, h) pairs
+    of the same workload.  Codes are drawn uniformly by the input generator
+    (the oracle's running time does not depend on their values); P comes from
+    the oracle's own build on the first 256 keys of the head."""
+    import numpy as np
+    import torch
+    from threadpoolctl import threadpool_limits
+
+    import oracle
+
+    def bits(t):
+        return t.detach().cpu().contiguous().view(torch.int16).numpy().view(np.uint16)
+
+    rng = np.random.default_rng(7)
+    sm = 1.0 / math.sqrt(cfg.D)
+    G = inst["G"].cpu().numpy()
+    total = 0.0
+    pairs = [(b, h) for b in range(cfg.B) for h in range(cfg.Hkv)][:heads]
+    with threadpool_limits(1):
+        for b, h in pairs:
+            K = bits(inst["K"][b, h])
+            V = bits(inst["V"][b, h])
+            q = bits(inst["q"][b, h * cfg.G:(h + 1) * cfg.G])
+            codes = rng.integers(0, 1 << 32, size=(cfg.N, cfg.L // 32), dtype=np.uint64).astype(np.uint32)
+            P = oracle.build_binary_pcs(K[:256], G)[0]
+            t0 = time.perf_counter()
+            oracle.decode_head(q, K, V, codes, P, cfg.k, sm)
+            total += time.perf_counter() - t0
+    keys = len(pairs) * cfg.N
+    return {"value": keys / total, "unit": "keys/s", "cores": 1, "kind": "oracle",
+            "sample": f"decode step of {len(pairs)} of the {cfg.B * cfg.Hkv} (sequence, KV head) pairs "
+                      f"({keys} keys) of {cfg.name}, numpy fp64 oracle on one thread, {total:.1f} s"}
+
+
+if __name__ == "__main__":
+    main()

@@ -78,6 +78,7 @@ DecodeLayout decode_layout(int B, int Hq, int Hkv, int N, int L, int k) {
   d.G = Hq / Hkv;
   d.nslices = (N + kSlice - 1) / kSlice;
   d.nchunks = (k + kAttnChunk - 1) / kAttnChunk;
+  const size_t S = BH * d.nslices;
   size_t o = 0;
   auto take = [&](size_t bytes) {
     size_t at = o;
@@ -86,15 +87,15 @@ DecodeLayout decode_layout(int B, int Hq, int Hkv, int N, int L, int k) {
   };
   d.off_qcode = take(BH * 8 * d.W * sizeof(uint32_t));
   d.off_T = take(BH * sizeof(int32_t));
-  d.off_cand = take(BH * d.nslices * (size_t)kSlice * sizeof(uint32_t));
-  d.off_cand_count = take(BH * d.nslices * sizeof(int32_t));
-  d.off_hist_fine = take(BH * d.nslices * (size_t)fine_stride(L) * sizeof(uint16_t));
-  d.off_hist_coarse = take(BH * d.nslices * (size_t)kCoarseBins * sizeof(uint32_t));
+  d.off_cand = take(S * (size_t)kSlice * sizeof(uint32_t));
+  d.off_cand_count = take(S * sizeof(int32_t));
+  d.off_hist_fine = take(S * (size_t)fine_stride(L) * sizeof(uint32_t));
+  d.off_hist_cc = take(S * (size_t)kCoarseStride * sizeof(uint32_t));
   d.off_sel_info = take(BH * 4 * sizeof(int32_t));
-  d.off_sel_base = take(BH * d.nslices * sizeof(int32_t));
-  d.off_tie_base = take(BH * d.nslices * sizeof(int32_t));
+  d.off_sel_base = take(S * sizeof(int32_t));
+  d.off_tie_base = take(S * sizeof(int32_t));
   d.off_idx = take(BH * (size_t)k * sizeof(int32_t));
-  d.off_part = take(BH * d.nchunks * (size_t)d.G * (kHeadDim + 2) * sizeof(float));
+  d.off_part = take(BH * (size_t)d.nchunks * d.G * (kHeadDim + 2) * sizeof(float));
   d.total = o;
   return d;
 }

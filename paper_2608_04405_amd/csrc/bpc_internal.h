@@ -19,25 +19,32 @@ constexpr int kHeadDim = 128;
 // (sequence, KV head); the slice's distances stay in LDS.
 constexpr int kSlice = 16384;
 constexpr int kScanThreads = 1024;
-// Selected keys attended by one attention workgroup.
-constexpr int kAttnChunk = 256;
+// One attention workgroup gathers kAttnChunk selected rows of one
+// (sequence, KV head): four wavefronts of 32 rows each.
+constexpr int kAttnChunk = 128;
 constexpr int kAttnThreads = 256;
+constexpr int kSelectThreads = 256;
 constexpr int kCoarseShift = 7;  // coarse histogram bin = distance >> 7
 constexpr int kCoarseBins = 128;
 constexpr int kMaxGroup = 16;  // query heads per KV head
 
 // Weighted Hamming distances lie in [0, 127 L].
 __host__ __device__ constexpr int dist_bins(int L) { return 127 * L + 1; }
-// Per-slice fine-histogram stride (u16 counts), padded to 16 bytes.
-__host__ __device__ constexpr int fine_stride(int L) { return (dist_bins(L) + 7) & ~7; }
+// Per-slice fine histogram: one u32 per distance bin, (count of keys with
+// distance in [128 * (t >> 7), t)) << 16 | (count at t); stride padded to
+// 16 bytes.  Per-slice coarse prefix: 129 u32 (keys with distance < 128 c),
+// stride kCoarseStride.
+__host__ __device__ constexpr int fine_stride(int L) { return (dist_bins(L) + 3) & ~3; }
+constexpr int kCoarseStride = 132;
 
 // ---- build tiling ----------------------------------------------------------
 constexpr int kBuildRows = 256;  // rows per workgroup in the build passes
 
 // ---- workspace layouts -----------------------------------------------------
 struct DecodeLayout {
-  int nslices, nchunks, G, W;
-  size_t off_qcode, off_T, off_cand, off_cand_count, off_hist_fine, off_hist_coarse,
+  int nslices, G, W;
+  int nchunks;
+  size_t off_qcode, off_T, off_cand, off_cand_count, off_hist_fine, off_hist_cc,
       off_sel_info, off_sel_base, off_tie_base, off_idx, off_part, total;
 };
 
