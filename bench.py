@@ -47,6 +47,9 @@ def parse():
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run a plain 1 GiB device copy (counter calibration for rocprofv3 --pmc)")
     ap.add_argument("--cpu-sample-heads", type=int, default=64)
+    ap.add_argument("--summarize", metavar="DIR", default=None,
+                    help="summarize rocprofv3 csv output under DIR (kernel stats and counters per dispatch) "
+                         "instead of benchmarking")
     return ap.parse_args()
 
 
@@ -61,8 +64,50 @@ def source_sha() -> str:
     return h.hexdigest()[:16]
 
 
+def summarize(root: str) -> None:
+    """Per-kernel summary of rocprofv3 csv output (kernel stats, and the mean
+    of every collected counter per dispatch)."""
+    import csv
+    import glob
+    from collections import defaultdict
+
+    def short(name):
+        name = name.split("(")[0]
+        return name.replace("void ", "").strip()
+
+    lines = []
+    for f in sorted(glob.glob(os.path.join(root, "**", "*kernel_stats.csv"), recursive=True)):
+        lines.append(f"kernel stats ({os.path.relpath(f, root)}):")
+        lines.append(f"{'kernel':<48}{'calls':>8}{'avg_us':>12}{'total_ms':>12}")
+        for r in csv.DictReader(open(f)):
+            if "bpc::" in r["Name"] or "copyBuffer" in r["Name"] or "elementwise" in r["Name"] and "copy" in r["Name"]:
+                lines.append(f"{short(r['Name'])[:47]:<48}{int(r['Calls']):>8}{float(r['AverageNs']) / 1e3:>12.2f}"
+                             f"{float(r['TotalDurationNs']) / 1e6:>12.3f}")
+    for f in sorted(glob.glob(os.path.join(root, "**", "*counter_collection.csv"), recursive=True)):
+        acc = defaultdict(lambda: defaultdict(list))
+        rows = [r for r in csv.DictReader(open(f))
+                if "bpc::" in r.get("Kernel_Name", "") or "copyBuffer" in r.get("Kernel_Name", "")]
+        # copy kernels: only the largest dispatches (the 1 GiB calibration copy)
+        gmax = max((int(r.get("Grid_Size", 0) or 0) for r in rows if "copyBuffer" in r["Kernel_Name"]), default=0)
+        for r in rows:
+            name = r["Kernel_Name"]
+            if "copyBuffer" in name:
+                if int(r.get("Grid_Size", 0) or 0) != gmax:
+                    continue
+                name = f"{short(name)} (grid {gmax})"
+            acc[short(name)][r["Counter_Name"]].append(float(r["Counter_Value"]))
+        lines.append(f"counters, mean per dispatch ({os.path.relpath(f, root)}):")
+        for k in sorted(acc):
+            vals = ", ".join(f"{c}={sum(v) / len(v):.6g} (n={len(v)})" for c, v in sorted(acc[k].items()))
+            lines.append(f"  {k}: {vals}")
+    print("\n".join(lines))
+
+
 def main():
     args = parse()
+    if args.summarize:
+        summarize(args.summarize)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (the decode step of every "
               "(sequence, KV head) is independent; see DESIGN.md for how it would shard).", file=sys.stderr)

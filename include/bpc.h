@@ -182,11 +182,11 @@ int bpc_decode_attention(const uint16_t* q,
 /*
  * bpc_decode_attention_profiled -- bpc_decode_attention that also records
  * caller-created hipEvent_t handles on `stream` at the stage boundaries
- * (query packing | scoring | threshold | selection | attention | merge):
+ * (query packing | scoring | threshold and selection | attention | merge):
  * events[0] before the first stage and events[s + 1] after stage s, so
  * n_events must be BPC_DECODE_STAGES + 1.  For measuring only.
  */
-#define BPC_DECODE_STAGES 6
+#define BPC_DECODE_STAGES 5
 int bpc_decode_attention_profiled(const uint16_t* q,
                                   const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t sK_n,
                                   const uint16_t* V, int64_t sV_b, int64_t sV_h, int64_t sV_n,

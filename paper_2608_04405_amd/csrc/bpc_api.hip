@@ -91,9 +91,6 @@ DecodeLayout decode_layout(int B, int Hq, int Hkv, int N, int L, int k) {
   d.off_cand_count = take(S * sizeof(int32_t));
   d.off_hist_fine = take(S * (size_t)fine_stride(L) * sizeof(uint32_t));
   d.off_hist_cc = take(S * (size_t)kCoarseStride * sizeof(uint32_t));
-  d.off_sel_info = take(BH * 4 * sizeof(int32_t));
-  d.off_sel_base = take(S * sizeof(int32_t));
-  d.off_tie_base = take(S * sizeof(int32_t));
   d.off_idx = take(BH * (size_t)k * sizeof(int32_t));
   d.off_part = take(BH * (size_t)d.nchunks * d.G * (kHeadDim + 2) * sizeof(float));
   d.total = o;
@@ -220,6 +217,10 @@ static int decode_impl(const uint16_t* q, const uint16_t* K, int64_t sK_b, int64
   if (!aligned16(q) || !aligned16(out)) return fail(BPC_EALIGN, "q and out must be 16-byte aligned");
   if ((st = check_kv("K", K, sK_b, sK_h, sK_n))) return st;
   if ((st = check_kv("V", V, sV_b, sV_h, sV_n))) return st;
+  // the attention kernel addresses a row by a 32-bit byte offset within its head
+  if ((int64_t)(N - 1) * sK_n * 2 + 256 > (int64_t)UINT32_MAX || (int64_t)(N - 1) * sV_n * 2 + 256 > (int64_t)UINT32_MAX)
+    return fail(BPC_EUNSUPPORTED, "the N rows of one head must span less than 4 GiB (N=%d, row strides %lld, %lld)",
+                N, (long long)sK_n, (long long)sV_n);
   if ((st = check_codes("codes", codes, sC_b, sC_h, L / 32))) return st;
   if ((st = check_proj(P, sP_b, sP_h))) return st;
   if ((st = check_opt_aligned("idx_out", idx_out))) return st;

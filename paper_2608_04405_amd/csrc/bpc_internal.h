@@ -44,8 +44,7 @@ constexpr int kBuildRows = 256;  // rows per workgroup in the build passes
 struct DecodeLayout {
   int nslices, G, W;
   int nchunks;
-  size_t off_qcode, off_T, off_cand, off_cand_count, off_hist_fine, off_hist_cc,
-      off_sel_info, off_sel_base, off_tie_base, off_idx, off_part, total;
+  size_t off_qcode, off_T, off_cand, off_cand_count, off_hist_fine, off_hist_cc, off_idx, off_part, total;
 };
 
 struct BuildLayout {
