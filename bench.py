@@ -46,10 +46,12 @@ def parse():
     ap.add_argument("--no-prefill", action="store_true")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run a plain 1 GiB device copy (counter calibration for rocprofv3 --pmc)")
-    ap.add_argument("--cpu-sample-heads", type=int, default=64)
-    ap.add_argument("--summarize", metavar="DIR", default=None,
-                    help="summarize rocprofv3 csv output under DIR (kernel stats and counters per dispatch) "
+    ap.add_argument("--cpu-sample-heads", type=int, default=128)
+    ap.add_argument("--summarize", metavar="DIR", nargs="+", default=None,
+                    help="summarize rocprofv3 csv output under each DIR (kernel stats and counters per dispatch) "
                          "instead of benchmarking")
+    ap.add_argument("--pmc-json", metavar="PATH", default=None,
+                    help="with --summarize over a FETCH_SIZE and a WRITE_SIZE run: write HBM bytes per launch")
     return ap.parse_args()
 
 
@@ -58,55 +60,109 @@ def log(msg):
 
 
 def source_sha() -> str:
+    """Hash of the decode kernels' source with comments and blank lines
+    removed: counter readings stay valid across comment-only edits."""
+    import re
     h = hashlib.sha256()
     for p in KERNEL_SOURCES:
-        h.update(open(p, "rb").read())
+        for line in open(p).read().splitlines():
+            line = re.sub(r"//.*", "", line).strip()
+            if line:
+                h.update(line.encode() + b"\n")
     return h.hexdigest()[:16]
 
 
-def summarize(root: str) -> None:
-    """Per-kernel summary of rocprofv3 csv output (kernel stats, and the mean
-    of every collected counter per dispatch)."""
+def _short(name: str) -> str:
+    return name.split("(")[0].replace("void ", "").strip()
+
+
+def _is_copy(name: str) -> bool:
+    return "copyBuffer" in name
+
+
+def _stage_of(name: str):
+    import re
+    m = re.search(r"bpc::(\w+?)_kernel", name)
+    return m.group(1) if m else None
+
+
+def summarize(roots, pmc_json=None) -> None:
+    """Per-kernel summary of rocprofv3 csv output under each of `roots`
+    (kernel stats, and the mean of every collected counter per dispatch).
+
+    With `pmc_json`, the FETCH_SIZE / WRITE_SIZE means (KiB per dispatch) of
+    the library's kernels are converted to HBM bytes per launch and written
+    there.  Each counter is scaled by the factor that makes it read the
+    known size of the 1 GiB device copies that `--copy-probe` adds to the
+    run (the largest copy dispatches of the run; their read and their write
+    are 1 GiB each)."""
     import csv
     import glob
     from collections import defaultdict
 
-    def short(name):
-        name = name.split("(")[0]
-        return name.replace("void ", "").strip()
-
     lines = []
-    for f in sorted(glob.glob(os.path.join(root, "**", "*kernel_stats.csv"), recursive=True)):
-        lines.append(f"kernel stats ({os.path.relpath(f, root)}):")
-        lines.append(f"{'kernel':<48}{'calls':>8}{'avg_us':>12}{'total_ms':>12}")
-        for r in csv.DictReader(open(f)):
-            if "bpc::" in r["Name"] or "copyBuffer" in r["Name"] or "elementwise" in r["Name"] and "copy" in r["Name"]:
-                lines.append(f"{short(r['Name'])[:47]:<48}{int(r['Calls']):>8}{float(r['AverageNs']) / 1e3:>12.2f}"
-                             f"{float(r['TotalDurationNs']) / 1e6:>12.3f}")
-    for f in sorted(glob.glob(os.path.join(root, "**", "*counter_collection.csv"), recursive=True)):
-        acc = defaultdict(lambda: defaultdict(list))
-        rows = [r for r in csv.DictReader(open(f))
-                if "bpc::" in r.get("Kernel_Name", "") or "copyBuffer" in r.get("Kernel_Name", "")]
-        # copy kernels: only the largest dispatches (the 1 GiB calibration copy)
-        gmax = max((int(r.get("Grid_Size", 0) or 0) for r in rows if "copyBuffer" in r["Kernel_Name"]), default=0)
-        for r in rows:
-            name = r["Kernel_Name"]
-            if "copyBuffer" in name:
-                if int(r.get("Grid_Size", 0) or 0) != gmax:
-                    continue
-                name = f"{short(name)} (grid {gmax})"
-            acc[short(name)][r["Counter_Name"]].append(float(r["Counter_Value"]))
-        lines.append(f"counters, mean per dispatch ({os.path.relpath(f, root)}):")
-        for k in sorted(acc):
-            vals = ", ".join(f"{c}={sum(v) / len(v):.6g} (n={len(v)})" for c, v in sorted(acc[k].items()))
-            lines.append(f"  {k}: {vals}")
+    kernels = defaultdict(dict)   # stage -> counter -> mean KiB per dispatch
+    calib = {}                    # counter -> (mean KiB of the 1 GiB copies, n)
+    for root in roots:
+        for f in sorted(glob.glob(os.path.join(root, "**", "*kernel_stats.csv"), recursive=True)):
+            lines.append(f"kernel stats ({os.path.relpath(f, root)}):")
+            lines.append(f"{'kernel':<48}{'calls':>8}{'avg_us':>12}{'min_us':>10}{'max_us':>10}{'total_ms':>12}")
+            for r in csv.DictReader(open(f)):
+                if "bpc::" in r["Name"] or _is_copy(r["Name"]):
+                    lines.append(f"{_short(r['Name'])[:47]:<48}{int(r['Calls']):>8}"
+                                 f"{float(r['AverageNs']) / 1e3:>12.2f}{float(r.get('MinNs', 'nan')) / 1e3:>10.2f}"
+                                 f"{float(r.get('MaxNs', 'nan')) / 1e3:>10.2f}{float(r['TotalDurationNs']) / 1e6:>12.3f}")
+        for f in sorted(glob.glob(os.path.join(root, "**", "*counter_collection.csv"), recursive=True)):
+            acc = defaultdict(lambda: defaultdict(list))
+            copies = defaultdict(list)
+            for r in csv.DictReader(open(f)):
+                name = r.get("Kernel_Name", "")
+                val = float(r["Counter_Value"])
+                if _is_copy(name):
+                    copies[r["Counter_Name"]].append(val)
+                elif "bpc::" in name:
+                    acc[_short(name)][r["Counter_Name"]].append(val)
+            lines.append(f"counters, mean per dispatch ({os.path.relpath(f, root)}):")
+            for cname, vals in sorted(copies.items()):
+                # the calibration copies are by far the largest copies of the run
+                big = [v for v in vals if v >= 0.5 * max(vals)]
+                calib[cname] = (sum(big) / len(big), len(big))
+                lines.append(f"  1 GiB device copy: {cname}={calib[cname][0]:.6g} (n={len(big)})")
+            for kname in sorted(acc):
+                vals = ", ".join(f"{c}={sum(v) / len(v):.6g} (n={len(v)})" for c, v in sorted(acc[kname].items()))
+                lines.append(f"  {kname}: {vals}")
+                st = _stage_of(kname)
+                if st:
+                    for c, v in acc[kname].items():
+                        kernels[st][c] = sum(v) / len(v)
     print("\n".join(lines))
+    if pmc_json:
+        need = ("FETCH_SIZE", "WRITE_SIZE")
+        if not all(c in calib for c in need):
+            raise SystemExit("FETCH_SIZE and WRITE_SIZE runs with --copy-probe are both needed")
+        factor = {c: float(1 << 30) / (calib[c][0] * 1024.0) for c in need}
+        out = {"source_sha": source_sha(),
+               "counter_unit": "KiB per dispatch",
+               "copy_calibration": {c: {"copy_bytes": 1 << 30, "counter_kib": calib[c][0], "dispatches": calib[c][1],
+                                        "bytes_per_counted_kib": factor[c] * 1024.0} for c in need},
+               "kernels": {}}
+        for st, cs in sorted(kernels.items()):
+            if all(c in cs for c in need):
+                fb = cs["FETCH_SIZE"] * 1024.0 * factor["FETCH_SIZE"]
+                wb = cs["WRITE_SIZE"] * 1024.0 * factor["WRITE_SIZE"]
+                out["kernels"][st] = {"fetch_kib": cs["FETCH_SIZE"], "write_kib": cs["WRITE_SIZE"],
+                                      "read_bytes": round(fb), "write_bytes": round(wb),
+                                      "hbm_bytes_per_launch": round(fb + wb)}
+        with open(pmc_json, "w") as fh:
+            json.dump(out, fh, indent=1)
+            fh.write("\n")
+        print(f"wrote {pmc_json}")
 
 
 def main():
     args = parse()
     if args.summarize:
-        summarize(args.summarize)
+        summarize(args.summarize, args.pmc_json)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (the decode step of every "

@@ -592,12 +592,12 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(int k, int nslic
 }
 
 // ---------------------------------------------------------------------------
-// 5. attention over the selected rows -- one workgroup per 128 selected keys
+// 4. attention over the selected rows -- one workgroup per 128 selected keys
 // Sixteen lanes share a key row (lane l16 holds dims [8 l16, 8 l16 + 8)),
 // four rows per wavefront instruction, 32 rows per wavefront; the wavefront
 // loads its 32 row indices once and issues every K and V row load before
 // the first is consumed.  Logits are kept in base 2 (sm_scale * log2 e).
-// The last workgroup of a (b, h) to finish merges the chunk partials.
+// Each workgroup writes one (max, sum, weighted V) partial per query head.
 // ---------------------------------------------------------------------------
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 
@@ -790,7 +790,7 @@ __global__ __launch_bounds__(kAttnThreads) void attend_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// 6. merge -- one workgroup per (b, query head): log-sum-exp combination of
+// 5. merge -- one workgroup per (b, query head): log-sum-exp combination of
 // the chunk partials.  A separate launch (rather than a last-workgroup
 // merge inside the attention kernel) because making the partials visible
 // across the chip from inside a kernel needs a device-scope release per

@@ -1,0 +1,173 @@
+"""Full-size parity: the HIP path at the workloads' real shapes, launched
+exactly as the benchmark launches it (the whole batch in one call, the
+library's own workspace sizing), checked against the oracle on sampled
+outputs that the oracle can afford, and through properties on every head.
+
+* batch16_128k (batch 16, 32/8 heads, 131072 keys, 64-bit codes, top-2622):
+  GPU build + decode of the whole batch; one sampled (sequence, KV head) is
+  rebuilt by the oracle (projection and codes bit-exact) and decoded by the
+  oracle (query planes, scores, indices bit-exact; output within 2e-3).
+* stack32_b8_64k, one layer (batch 8, 65536 keys, top-1311): the same for the
+  build, plus Algorithm 2 on sampled keys (each key hashes independently).
+* million_1m (1 048 576 keys, 128-bit codes, top-10486): the oracle cannot
+  build over a million keys in test time, so the decode takes seeded random
+  codes and projections the oracle built over a 2048-key prefix of each head;
+  two heads are decoded by the oracle; Algorithm 2 is checked on sampled keys
+  of the full cache.
+
+Every head, sampled or not, is checked for the selection property: indices
+strictly ascending, and the selected keys are the k best by score with equal
+scores going to the lower index.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from workloads import config_by_name, make_layer
+
+pytestmark = pytest.mark.gpu
+
+if torch.cuda.is_available():
+    import paper_2608_04405_amd as bpc
+else:  # pragma: no cover
+    bpc = None
+
+DEV = "cuda"
+TOL = 2e-3
+
+
+def bits(t):
+    return t.detach().cpu().contiguous().view(torch.int16).numpy().view(np.uint16)
+
+
+def u32(t):
+    return t.detach().cpu().contiguous().numpy().view(np.uint32)
+
+
+def rel_err(o, ref):
+    o = np.asarray(o, np.float64)
+    return np.max(np.abs(o - ref), axis=-1) / np.max(np.abs(ref), axis=-1)
+
+
+def announce(msg):
+    print(msg, flush=True)
+
+
+def check_selection_property(scores: np.ndarray, idx: np.ndarray, k: int, where: str) -> None:
+    """idx ascending, unique, in range; {scores[idx]} are the k largest with
+    ties at the threshold resolved towards the lower index."""
+    N = scores.shape[0]
+    assert idx.shape == (k,), where
+    assert idx[0] >= 0 and idx[-1] < N and np.all(np.diff(idx) > 0), f"{where}: indices not ascending/in range"
+    sel = np.zeros(N, bool)
+    sel[idx] = True
+    if k == N:
+        return
+    s_min = scores[sel].min()
+    u_max = scores[~sel].max()
+    assert s_min >= u_max, f"{where}: an unselected key outscores a selected one"
+    if s_min == u_max:
+        tied_sel = np.flatnonzero(sel & (scores == s_min))
+        tied_uns = np.flatnonzero(~sel & (scores == s_min))
+        assert tied_sel.max() < tied_uns.min(), f"{where}: tie at the threshold not broken by lowest index"
+
+
+def decode_full(q, K, V, codes, P, k, N):
+    B, Hq, _ = q.shape
+    Hkv = K.shape[1]
+    L = P.shape[-2]
+    idx = torch.empty(B, Hkv, k, dtype=torch.int32, device=DEV)
+    sc = torch.empty(B, Hkv, N, dtype=torch.int32, device=DEV)
+    qc = torch.empty(B, Hkv, 8, L // 32, dtype=torch.int32, device=DEV)
+    out = bpc.decode_attention(q, K, V, codes, P, k, N=N, idx_out=idx, score_out=sc, qcode_out=qc)
+    torch.cuda.synchronize()
+    return out, idx, sc, qc
+
+
+def all_heads_property(sc, idx, k):
+    scn = sc.cpu().numpy()
+    idn = idx.cpu().numpy()
+    B, Hkv = idn.shape[:2]
+    for b in range(B):
+        for h in range(Hkv):
+            check_selection_property(scn[b, h], idn[b, h], k, f"head {(b, h)}")
+
+
+def compare_sampled_head(d, P_ref, codes_ref, b, h, cfg, out, idx, sc, qc, label):
+    Gq = cfg.G
+    sm = 1.0 / np.sqrt(cfg.D)
+    qb = bits(d["q"][b, h * Gq:(h + 1) * Gq])
+    Kb = bits(d["K"][b, h, :cfg.N])
+    Vb = bits(d["V"][b, h, :cfg.N])
+    ref = oracle.decode_head(qb, Kb, Vb, codes_ref, P_ref, cfg.k, sm)
+    assert np.array_equal(u32(qc[b, h]), ref["qcode"]), f"{label}: query planes differ"
+    assert np.array_equal(sc[b, h].cpu().numpy(), ref["scores"]), f"{label}: scores differ"
+    assert np.array_equal(idx[b, h].cpu().numpy(), ref["idx"]), f"{label}: indices differ"
+    e = rel_err(out[b, h * Gq:(h + 1) * Gq].cpu().numpy(), ref["out"])
+    announce(f"{label}: max relative output error {e.max():.3g}")
+    assert np.all(e <= TOL), f"{label}: output error {e.max():.3g}"
+
+
+def build_decode_case(name, sample, hash_rows):
+    cfg = config_by_name(name)
+    announce(f"[full size] {cfg}")
+    d = make_layer(cfg, device=DEV)
+    G = d["G"].to(DEV)
+    P, codes, err = bpc.build_hash(d["K"], G, err_out=torch.empty(cfg.B, cfg.Hkv, cfg.N, device=DEV))
+    out, idx, sc, qc = decode_full(d["q"], d["K"], d["V"], codes, P, cfg.k, cfg.N)
+    assert torch.isfinite(out).all()
+    all_heads_property(sc, idx, cfg.k)
+    b, h = sample
+    Kb = bits(d["K"][b, h, :cfg.N])
+    announce(f"[full size] oracle build of head {(b, h)} over {cfg.N} keys")
+    P_ref, codes_ref, err_ref, _ = oracle.build_binary_pcs(Kb, d["G"].numpy())
+    assert np.array_equal(P[b, h].cpu().numpy(), P_ref), f"{name}: projection differs at {(b, h)}"
+    assert np.array_equal(u32(codes[b, h]), codes_ref), f"{name}: codes differ at {(b, h)}"
+    np.testing.assert_allclose(err[b, h].cpu().numpy(), err_ref, rtol=1e-5, atol=1e-4)
+    compare_sampled_head(d, P_ref, codes_ref, b, h, cfg, out, idx, sc, qc, f"{name} head {(b, h)}")
+    if hash_rows:
+        rng = np.random.default_rng(cfg.seed)
+        rows = np.unique(np.concatenate([rng.choice(cfg.N, hash_rows, replace=False), [0, cfg.N - 1]]))
+        c2, e2 = bpc.hash_keys(d["K"], P, err_out=torch.empty(cfg.B, cfg.Hkv, cfg.N, device=DEV))
+        torch.cuda.synchronize()
+        ref_codes, ref_err, _ = oracle.hash_keys(Kb[rows], P_ref)
+        assert np.array_equal(u32(c2[b, h])[rows], ref_codes), f"{name}: Algorithm 2 codes differ"
+        np.testing.assert_allclose(e2[b, h].cpu().numpy()[rows], ref_err, rtol=1e-5, atol=1e-4)
+
+
+@pytest.mark.timeout(600)
+def test_fullsize_batch16_128k():
+    build_decode_case("batch16_128k", sample=(11, 6), hash_rows=0)
+
+
+@pytest.mark.timeout(600)
+def test_fullsize_stack_layer_b8_64k():
+    build_decode_case("stack32_b8_64k", sample=(5, 2), hash_rows=1024)
+
+
+@pytest.mark.timeout(600)
+def test_fullsize_million_1m():
+    cfg = config_by_name("million_1m")
+    announce(f"[full size] {cfg}")
+    d = make_layer(cfg, device=DEV)
+    Gn = d["G"].numpy()
+    rng = np.random.default_rng(cfg.seed)
+    prefix = 2048
+    P_np = np.stack([oracle.build_binary_pcs(bits(d["K"][0, h, :prefix]), Gn)[0] for h in range(cfg.Hkv)])[None]
+    codes_np = rng.integers(0, 1 << 32, size=(cfg.B, cfg.Hkv, cfg.N, cfg.W), dtype=np.uint64).astype(np.uint32)
+    codes = torch.from_numpy(codes_np.view(np.int32)).to(DEV)
+    P = torch.from_numpy(P_np).to(DEV)
+    out, idx, sc, qc = decode_full(d["q"], d["K"], d["V"], codes, P, cfg.k, cfg.N)
+    assert torch.isfinite(out).all()
+    all_heads_property(sc, idx, cfg.k)
+    for h in (0, 7):
+        compare_sampled_head(d, P_np[0, h], codes_np[0, h], 0, h, cfg, out, idx, sc, qc, f"million head {h}")
+    # Algorithm 2 over the whole million-key cache, checked on sampled keys
+    c2, _ = bpc.hash_keys(d["K"], P)
+    torch.cuda.synchronize()
+    rows = np.unique(np.concatenate([rng.choice(cfg.N, 512, replace=False), [0, cfg.N - 1]]))
+    for h in (3,):
+        ref_codes, _, _ = oracle.hash_keys(bits(d["K"][0, h])[rows], P_np[0, h])
+        assert np.array_equal(u32(c2[0, h])[rows], ref_codes), "million: Algorithm 2 codes differ"
