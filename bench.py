@@ -272,10 +272,10 @@ def main():
     p_bytes = BH * L * D * 4
     qo_bytes = B * Hq * D * (2 + 4)
     step_bytes = code_bytes + gather_bytes + p_bytes + qo_bytes
-    per_kernel_bytes = {"scan": code_bytes, "attend": gather_bytes + B * Hq * D * 2,
+    per_kernel_bytes = {"score": code_bytes, "attend": gather_bytes + B * Hq * D * 2,
                         "qpack": p_bytes + B * Hq * D * 2}
     # dominant kernel: the stage with the largest time among the HBM streamers
-    dom = max(("scan", "attend"), key=lambda n: stages[n])
+    dom = max(("score", "attend"), key=lambda n: stages[n])
     dom_us = stages[dom]
     achieved = per_kernel_bytes[dom] / (dom_us * 1e-6) / 1e9
     traffic = None

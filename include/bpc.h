@@ -156,13 +156,17 @@ int bpc_hash_keys(const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t sK_n,
  *            (sV_b, sV_h, sV_n)
  * codes      [B, Hkv, >=N, W] uint32, strides sC_b, sC_h
  * P          [B, Hkv, L, D] fp32, strides sP_b, sP_h (0, 0 = shared)
+ * N          1 <= N <= 16777216 cached keys per (b, KV head)
  * k          1 <= k <= N selected keys per (b, KV head)
  * out        [B, Hq, D] fp32, contiguous (written)
  * idx_out    [B, Hkv, k] int32 selected key indices, ascending (or NULL)
  * score_out  [B, Hkv, N] int32 scores c_n (or NULL)
  * qcode_out  [B, Hkv, 8, W] uint32 packed query planes (or NULL)
  * workspace  at least bpc_decode_workspace_bytes(...) bytes, 256-byte
- *            aligned; contents on entry do not matter.
+ *            aligned; contents on entry do not matter.  Two calls that use
+ *            the same workspace must be ordered on one stream.
+ * Cost: four kernel launches (query packing, scoring, threshold with
+ * selection and attention, merge of the per-slice partials).
  */
 size_t bpc_decode_workspace_bytes(int B, int Hq, int Hkv, int N, int D, int L, int k);
 int bpc_decode_attention(const uint16_t* q,
@@ -182,11 +186,11 @@ int bpc_decode_attention(const uint16_t* q,
 /*
  * bpc_decode_attention_profiled -- bpc_decode_attention that also records
  * caller-created hipEvent_t handles on `stream` at the stage boundaries
- * (query packing | scoring | threshold and selection | attention | merge):
+ * (query packing | scoring | threshold, selection and attention | merge):
  * events[0] before the first stage and events[s + 1] after stage s, so
  * n_events must be BPC_DECODE_STAGES + 1.  For measuring only.
  */
-#define BPC_DECODE_STAGES 5
+#define BPC_DECODE_STAGES 4
 int bpc_decode_attention_profiled(const uint16_t* q,
                                   const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t sK_n,
                                   const uint16_t* V, int64_t sV_b, int64_t sV_h, int64_t sV_n,

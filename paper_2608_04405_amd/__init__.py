@@ -60,8 +60,8 @@ _lib.bpc_decode_attention.argtypes = _DECODE_ARGS
 _lib.bpc_decode_attention_profiled.restype = _i
 _lib.bpc_decode_attention_profiled.argtypes = _DECODE_ARGS + [ctypes.POINTER(_p), _i]
 
-DECODE_STAGES = 5
-DECODE_STAGE_NAMES = ("qpack", "scan", "select", "attend", "merge")
+DECODE_STAGES = 4
+DECODE_STAGE_NAMES = ("qpack", "score", "attend", "merge")
 
 
 class BPCError(RuntimeError):

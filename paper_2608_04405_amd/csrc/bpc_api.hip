@@ -77,7 +77,6 @@ DecodeLayout decode_layout(int B, int Hq, int Hkv, int N, int L, int k) {
   d.W = L / 32;
   d.G = Hq / Hkv;
   d.nslices = (N + kSlice - 1) / kSlice;
-  d.nchunks = (k + kAttnChunk - 1) / kAttnChunk;
   const size_t S = BH * d.nslices;
   size_t o = 0;
   auto take = [&](size_t bytes) {
@@ -85,14 +84,13 @@ DecodeLayout decode_layout(int B, int Hq, int Hkv, int N, int L, int k) {
     o = align_up(o + bytes, 256);
     return at;
   };
-  d.off_qcode = take(BH * 8 * d.W * sizeof(uint32_t));
-  d.off_T = take(BH * sizeof(int32_t));
   d.off_cand = take(S * (size_t)kSlice * sizeof(uint32_t));
-  d.off_cand_count = take(S * sizeof(int32_t));
+  d.off_meta = take(S * 4 * sizeof(uint32_t));
   d.off_hist_fine = take(S * (size_t)fine_stride(L) * sizeof(uint32_t));
   d.off_hist_cc = take(S * (size_t)kCoarseStride * sizeof(uint32_t));
+  d.off_part = take(S * d.G * (kHeadDim + 2) * sizeof(float));
   d.off_idx = take(BH * (size_t)k * sizeof(int32_t));
-  d.off_part = take(BH * (size_t)d.nchunks * d.G * (kHeadDim + 2) * sizeof(float));
+  d.off_qcode = take(BH * kQcodeStride * sizeof(uint32_t));
   d.total = o;
   return d;
 }
@@ -211,6 +209,8 @@ static int decode_impl(const uint16_t* q, const uint16_t* K, int64_t sK_b, int64
   if ((st = check_head_dim(D))) return st;
   if ((st = check_code_len(L))) return st;
   if (k < 1 || k > N) return fail(BPC_EINVAL, "k=%d must satisfy 1 <= k <= N=%d", k, N);
+  if ((int64_t)N > (int64_t)kMaxSlices * kSlice)
+    return fail(BPC_EUNSUPPORTED, "N=%d: decode supports at most %d cached keys per head", N, kMaxSlices * kSlice);
   if (!(sm_scale > 0.0f) || !__builtin_isfinite(sm_scale))
     return fail(BPC_EINVAL, "sm_scale must be finite and > 0");
   if (!q || !out) return fail(BPC_EINVAL, "q and out are required");

@@ -16,14 +16,16 @@ constexpr int kHeadDim = 128;
 
 // ---- decode tiling ---------------------------------------------------------
 // One scoring workgroup owns a slice of kSlice consecutive keys of one
-// (sequence, KV head); the slice's distances stay in LDS.
+// (sequence, KV head); the slice's distances stay in registers and its
+// histogram in LDS.  At most kMaxSlices slices per (sequence, KV head).
 constexpr int kSlice = 16384;
-constexpr int kScanThreads = 1024;
-// One attention workgroup gathers kAttnChunk selected rows of one
-// (sequence, KV head): four wavefronts of 32 rows each.
-constexpr int kAttnChunk = 128;
+constexpr int kScoreThreads = 512;  // scoring workgroup: 32 keys per thread
+constexpr int kScanThreads = 1024;  // query-packing workgroup
+constexpr int kMaxSlices = 1024;
+// One attention workgroup per slice keeps its selected candidates, read in
+// batches of kCandBatch, and gathers their rows with four wavefronts.
 constexpr int kAttnThreads = 256;
-constexpr int kSelectThreads = 256;
+constexpr int kCandBatch = 4096;
 constexpr int kCoarseShift = 7;  // coarse histogram bin = distance >> 7
 constexpr int kCoarseBins = 128;
 constexpr int kMaxGroup = 16;  // query heads per KV head
@@ -41,10 +43,17 @@ constexpr int kCoarseStride = 132;
 constexpr int kBuildRows = 256;  // rows per workgroup in the build passes
 
 // ---- workspace layouts -----------------------------------------------------
+// Decode, per slice sl = (b Hkv + h) nslices + s: candidates [kSlice] u32
+// (key-in-slice << 16 | distance), meta [4] u32 (kth_s, lowest occupied
+// coarse bin, candidate count), fine histogram [fine_stride] u32, coarse
+// prefix [kCoarseStride] u32 and G partials of (max, sum, o[128]) fp32; per
+// (b, h) the packed query (8 W plane words, then sum |p|; stride
+// kQcodeStride) and the k selected indices (used when the caller passes no
+// idx_out).
+constexpr int kQcodeStride = 64;
 struct DecodeLayout {
   int nslices, G, W;
-  int nchunks;
-  size_t off_qcode, off_T, off_cand, off_cand_count, off_hist_fine, off_hist_cc, off_idx, off_part, total;
+  size_t off_cand, off_meta, off_hist_fine, off_hist_cc, off_part, off_idx, off_qcode, total;
 };
 
 struct BuildLayout {

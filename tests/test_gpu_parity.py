@@ -278,6 +278,10 @@ def _random_case(rng, B, Hq, Hkv, N, L, Ncap=None, code_pool=None, qscale=1.0):
     dict(B=1, Hq=32, Hkv=4, N=20000, L=128, k=300, Ncap=20100),   # G = 8, strided cache
     dict(B=1, Hq=16, Hkv=16, N=3000, L=32, k=61),                 # G = 1
     dict(B=1, Hq=2, Hkv=1, N=70000, L=64, k=1400),                # G = 2, five slices
+    dict(B=1, Hq=4, Hkv=2, N=1001, L=32, k=30),                   # last 16-byte group holds one key
+    dict(B=2, Hq=4, Hkv=2, N=333, L=64, k=7, pool=5),             # odd key count, ties
+    dict(B=1, Hq=8, Hkv=2, N=65537, L=64, k=1311),                # ragged second run
+    dict(B=1, Hq=2, Hkv=1, N=1100000, L=32, k=50000, pool=40),    # over a million keys: three-kernel path
 ])
 def test_decode_edge_cases(case):
     announce(f"[decode edge] {case}")
@@ -285,6 +289,61 @@ def test_decode_edge_cases(case):
     q, K, V, codes, P = _random_case(rng, case["B"], case["Hq"], case["Hkv"], case["N"], case["L"], case.get("Ncap"),
                                      case.get("pool"))
     _decode_and_compare(q, K, V, codes, P, case["k"], N=case["N"], label=f"edge {case}")
+
+
+def test_decode_garbage_workspace():
+    """The workspace needs no clearing: a first call on random bytes, and
+    later calls on the same workspace, all match the oracle."""
+    rng = np.random.default_rng(21)
+    q, K, V, codes, P = _random_case(rng, 2, 8, 2, 40000, 64, code_pool=30)
+    B, Hq, Hkv, N, L, k = 2, 8, 2, 40000, 64, 800
+    ws = torch.randint(0, 256, (bpc.decode_workspace_bytes(B, Hq, Hkv, N, L, k),), dtype=torch.uint8, device=DEV)
+    cd = torch.from_numpy(codes.view(np.int32)).to(DEV)
+    Pd = torch.from_numpy(P).to(DEV)
+    outs = []
+    for _ in range(3):
+        idx = torch.empty(B, Hkv, k, dtype=torch.int32, device=DEV)
+        outs.append((bpc.decode_attention(q, K, V, cd, Pd, k, workspace=ws, idx_out=idx).clone(), idx))
+    torch.cuda.synchronize()
+    qb, Kb, Vb = bits(q), bits(K), bits(V)
+    for b in range(B):
+        for h in range(Hkv):
+            ref = oracle.decode_head(qb[b, 4 * h:4 * h + 4], Kb[b, h], Vb[b, h], codes[b, h], P[b, h], k,
+                                     1 / np.sqrt(128))
+            for out, idx in outs:
+                assert np.array_equal(idx[b, h].cpu().numpy(), ref["idx"])
+                assert np.all(rel_err(out[b, 4 * h:4 * h + 4].cpu().numpy(), ref["out"]) <= TOL)
+    assert all(torch.equal(outs[0][0], o) for o, _ in outs[1:])
+
+
+def test_decode_graph_replay():
+    """A decode step captured in a HIP graph gives the eager result on every
+    replay, with eager work and synchronisations between the replays."""
+    rng = np.random.default_rng(22)
+    q, K, V, codes, P = _random_case(rng, 2, 8, 2, 30000, 64)
+    k = 600
+    cd = torch.from_numpy(codes.view(np.int32)).to(DEV)
+    Pd = torch.from_numpy(P).to(DEV)
+    ws = torch.empty(bpc.decode_workspace_bytes(2, 8, 2, 30000, 64, k), dtype=torch.uint8, device=DEV)
+    out = torch.empty(2, 8, 128, dtype=torch.float32, device=DEV)
+    eager = bpc.decode_attention(q, K, V, cd, Pd, k, out=torch.empty_like(out), workspace=ws).clone()
+    torch.cuda.synchronize()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(s):
+        bpc.decode_attention(q, K, V, cd, Pd, k, out=out, workspace=ws, stream=s)  # warm-up on the side stream
+        s.synchronize()
+        with torch.cuda.graph(g, stream=s):
+            bpc.decode_attention(q, K, V, cd, Pd, k, out=out, workspace=ws, stream=s)
+    torch.cuda.synchronize()
+    for r in range(4):
+        out.zero_()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out, eager), f"replay {r} differs from the eager result"
+        bpc.decode_attention(q, K, V, cd, Pd, k, out=torch.empty_like(out), workspace=ws)  # eager work between
+        torch.cuda.synchronize()
 
 
 def test_decode_full_budget_is_full_attention():
