@@ -166,7 +166,8 @@ int bpc_hash_keys(const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t sK_n,
  *            aligned; contents on entry do not matter.  Two calls that use
  *            the same workspace must be ordered on one stream.
  * Cost: four kernel launches (query packing, scoring, threshold with
- * selection and attention, merge of the per-slice partials).
+ * selection and attention, merge of the per-slice partials), plus one for a
+ * ragged last slice or codes whose strides are not multiples of 4 words.
  */
 size_t bpc_decode_workspace_bytes(int B, int Hq, int Hkv, int N, int D, int L, int k);
 int bpc_decode_attention(const uint16_t* q,
