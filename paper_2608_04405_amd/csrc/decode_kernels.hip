@@ -31,6 +31,32 @@
 namespace bpc {
 
 // ---------------------------------------------------------------------------
+// Phase trace (only in builds with -DBPC_TRACE; the product build has none):
+// thread 0 of each workgroup stores the 100 MHz real-time counter at the
+// phase boundaries of its kernel into trace[(kernel * 65536 + workgroup) * 16
+// + slot] (slots 0..11), and a value of its own with BPC_NOTE (slots 12..15;
+// slot 15 = the XCC the workgroup ran on), in a buffer the host registers
+// with bpc_trace_buffer().
+// ---------------------------------------------------------------------------
+#ifdef BPC_TRACE
+__device__ unsigned long long* g_trace = nullptr;
+#define BPC_NOTE(kern, slot, val)                                                                \
+  do {                                                                                           \
+    if (threadIdx.x == 0 && g_trace && blockIdx.x < 65536)                                       \
+      g_trace[((size_t)(kern) * 65536 + blockIdx.x) * 16 + (slot)] = (unsigned long long)(val); \
+  } while (0)
+// hwreg(HW_REG_XCC_ID): bits 3:0 = the XCC of this wavefront
+#define BPC_STAMP(kern, slot)                                                                 \
+  do {                                                                                        \
+    BPC_NOTE(kern, slot, __builtin_amdgcn_s_memrealtime());                                   \
+    if ((slot) == 0) BPC_NOTE(kern, 15, __builtin_amdgcn_s_getreg((3 << 11) | 20) & 15);      \
+  } while (0)
+#else
+#define BPC_STAMP(kern, slot) ((void)0)
+#define BPC_NOTE(kern, slot, val) ((void)0)
+#endif
+
+// ---------------------------------------------------------------------------
 // block-wide exclusive scan of one int per thread (NT threads, wave64)
 // ---------------------------------------------------------------------------
 template <int NT>
@@ -158,9 +184,12 @@ __device__ __forceinline__ void qpack_body(QpackShared<L>& sh, const QpackRegs<L
     const bool valid = tr < ntriples;
     const int c = tr & 3, gi = valid ? (tr >> 2) : 0;
     const int g = gi / L, i = gi % L;
+    // each product of a bf16 query coordinate and an fp32 entry of P is
+    // exact in fp64 (8 + 24 significant bits), so the fused multiply-add
+    // rounds exactly as the separately rounded multiply and add would
     double acc = 0.0;
 #pragma unroll 8
-    for (int e = 0; e < 32; ++e) acc = dadd(acc, dmul((double)sh.P_s[i][c][e], (double)sh.q_s[g][c][e]));
+    for (int e = 0; e < 32; ++e) acc = __builtin_fma((double)sh.P_s[i][c][e], (double)sh.q_s[g][c][e], acc);
     const double s01 = dadd(acc, __shfl_xor(acc, 1, 64));
     const double a = dadd(s01, __shfl_xor(s01, 2, 64));
     if (valid && c == 0) sh.x_s[g][i] = a;
@@ -215,6 +244,7 @@ __global__ __launch_bounds__(kScanThreads) void qpack_kernel(const uint16_t* __r
   __shared__ uint32_t qc_s[8 * W];
   __shared__ int T_s;
   const int bh = blockIdx.x;
+  BPC_STAMP(0, 0);
   QpackRegs<L, kScanThreads> qr;
   qpack_load<L, kScanThreads>(qr, q, P, sP_b, sP_h, Hkv, G, bh);
   qpack_body<L, kScanThreads>(sh, qr, G, qc_s, &T_s);
@@ -225,6 +255,7 @@ __global__ __launch_bounds__(kScanThreads) void qpack_kernel(const uint16_t* __r
     if (qcode_out) qcode_out[(size_t)bh * 8 * W + threadIdx.x] = qc_s[threadIdx.x];
   }
   if (threadIdx.x == 0) dst[8 * W] = (uint32_t)T_s;
+  BPC_STAMP(0, 1);
 }
 
 // ---------------------------------------------------------------------------
@@ -362,6 +393,7 @@ __device__ __forceinline__ void score_body(ScoreShared<L>& sh, int bh, int s, co
     }
   }
   __syncthreads();
+  BPC_STAMP(1, 1);
   auto dist_of = [&](int it, int u) -> int {
     const int i = it * KPL + u;
     return (int)((dpk[i >> 1] >> ((i & 1) << 4)) & 0xFFFFu);
@@ -417,6 +449,7 @@ __device__ __forceinline__ void score_body(ScoreShared<L>& sh, int bh, int s, co
   }
   __syncthreads();
 
+  BPC_STAMP(1, 2);
   // wave 0: coarse prefix, the lowest occupied coarse bin, and the coarse bin
   // holding the slice's k-th key
   if (threadIdx.x < 64) {
@@ -455,6 +488,7 @@ __device__ __forceinline__ void score_body(ScoreShared<L>& sh, int bh, int s, co
   __syncthreads();
   const int kth = sh.kth;
   const int cmin = sh.cmin;
+  BPC_STAMP(1, 3);
 
   // ---- histograms for the threshold: coarse prefix (129 entries) and the
   // fine bins in [128 cmin, kth] (bins below are empty, bins above are never
@@ -545,8 +579,10 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(L
   const int64_t c0 = (int64_t)(bh / Hkv) * sC_b + (int64_t)(bh % Hkv) * sC_h + (int64_t)s * kSlice * (L / 32);
   const bool full = (s + 1) * kSlice <= N && (reinterpret_cast<uintptr_t>(codes + c0) & 15u) == 0;
   if (full != FULL) return;
+  BPC_STAMP(1, 0);
   score_body<L, FULL>(sh, bh, s, qcode_ws, codes, sC_b, sC_h, Hkv, N, k, nslices, cand, meta, hist_fine, hist_cc,
                       score_out);
+  BPC_STAMP(1, 4);
 }
 
 // ---------------------------------------------------------------------------
@@ -601,6 +637,7 @@ constexpr int kAttnWaves = kAttnThreads / 64;
 constexpr int kAttnSlots = 4;                // rows per lane per pass
 constexpr int kAttnRows = 4 * kAttnSlots;    // rows per wavefront per pass
 constexpr int kPlanCache = 16;               // slices whose histograms are kept in LDS
+constexpr int kRoundBatch = 8;               // histogram loads per thread issued together
 
 template <int G>
 struct AttendShared {
@@ -724,6 +761,7 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(G 
   const uint32_t* ccb = hist_cc + (size_t)bh * nslices * kCoarseStride;
   const uint32_t* hfb = hist_fine + (size_t)bh * nslices * FS;
   const uint32_t* mtb = meta + (size_t)bh * nslices * 4;
+  BPC_STAMP(2, 0);
 
   // the candidate count and the first batch of candidates load while the
   // threshold is derived (the candidate region always holds kSlice entries)
@@ -740,13 +778,25 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(G 
 
   // ---- a. threshold.  Round 1: GP(c + 1) = keys of all slices with coarse bin <= c
   // (its loads go first; the candidates and the queries load behind them)
+  // Each round's loads are issued together: kRoundBatch slices per thread
+  // at a time, the slice index clamped so every load is unconditional, and
+  // entries past the last slice dropped after the load.
   {
     const int c = threadIdx.x & (kCoarseBins - 1), grp = threadIdx.x >> 7;
     int acc = 0;
-    for (int u = grp; u < nslices; u += 2) {
-      const uint32_t v = ccb[(size_t)u * kCoarseStride + c + 1];
-      acc += (int)v;
-      if (cached) pl.cc[u][c + 1] = v;
+    for (int u0 = grp; u0 < nslices; u0 += 2 * kRoundBatch) {
+      uint32_t v[kRoundBatch];
+#pragma unroll
+      for (int j = 0; j < kRoundBatch; ++j)
+        v[j] = ccb[(size_t)min(u0 + 2 * j, nslices - 1) * kCoarseStride + c + 1];
+#pragma unroll
+      for (int j = 0; j < kRoundBatch; ++j) {
+        const int u = u0 + 2 * j;
+        if (u < nslices) {
+          acc += (int)v[j];
+          if (cached) pl.cc[u][c + 1] = v[j];
+        }
+      }
     }
     pl.part[grp][c] = acc;
     if (cached && threadIdx.x < nslices) {
@@ -771,6 +821,7 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(G 
   }
   __syncthreads();
   const int cstar = min(min(sh.first[0], sh.first[1]), kCoarseBins - 1);
+  BPC_STAMP(2, 1);
   const int below_c = (cstar > 0) ? pl.gp[cstar - 1] : 0;  // keys with coarse bin < c*
   __syncthreads();
   // Round 2: the fine bins of c*, summed over slices (bins a slice did not
@@ -778,19 +829,32 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(G 
   {
     const int j = threadIdx.x & ((1 << kCoarseShift) - 1), grp = threadIdx.x >> 7;
     const int t = (cstar << kCoarseShift) + j;
+    const int tc = min(t, NB - 1);
     int exc = 0, inc = 0;
-    for (int u = grp; u < nslices; u += 2) {
-      int kthu, cminu;
-      if (cached) {
-        kthu = pl.kth[u], cminu = pl.cmin[u];
-      } else {
-        const uint2 m = *reinterpret_cast<const uint2*>(mtb + u * 4);
-        kthu = (int)m.x, cminu = (int)m.y;
+    for (int u0 = grp; u0 < nslices; u0 += 2 * kRoundBatch) {
+      int kthu[kRoundBatch], cminu[kRoundBatch];
+      uint32_t v[kRoundBatch];
+#pragma unroll
+      for (int i = 0; i < kRoundBatch; ++i) {
+        const int u = min(u0 + 2 * i, nslices - 1);
+        if (cached) {
+          kthu[i] = pl.kth[u], cminu[i] = pl.cmin[u];
+        } else {
+          const uint2 m = *reinterpret_cast<const uint2*>(mtb + u * 4);
+          kthu[i] = (int)m.x, cminu[i] = (int)m.y;
+        }
+        v[i] = hfb[(size_t)u * FS + tc];  // a bin the slice did not write is dropped below
       }
-      const uint32_t v = (t < NB && t >= (cminu << kCoarseShift) && t <= kthu) ? hfb[(size_t)u * FS + t] : 0u;
-      if (cached) pl.fine[u][j] = v;
-      exc += (int)(v >> 16);
-      inc += (int)(v >> 16) + (int)(v & 0xFFFFu);
+#pragma unroll
+      for (int i = 0; i < kRoundBatch; ++i) {
+        const int u = u0 + 2 * i;
+        if (u < nslices) {
+          const uint32_t x = (t < NB && t >= (cminu[i] << kCoarseShift) && t <= kthu[i]) ? v[i] : 0u;
+          if (cached) pl.fine[u][j] = x;
+          exc += (int)(x >> 16);
+          inc += (int)(x >> 16) + (int)(x & 0xFFFFu);
+        }
+      }
     }
     pl.part[grp][j] = exc;
     pl.part2[grp][j] = inc;
@@ -806,6 +870,7 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(G 
   }
   __syncthreads();
   const int jt = min(min(sh.first[0], sh.first[1]), (1 << kCoarseShift) - 1);
+  BPC_STAMP(2, 2);
   const int tstar = min((cstar << kCoarseShift) + jt, NB - 1);
   const int need = k - (below_c + pl.gp[jt]);  // keys at T* to take, over all slices
   // Round 3: keys below T* and ties at T* of the slices before this one (and
@@ -847,6 +912,7 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(G 
   const int off = below_before + min(need, ties_before);
   (void)my_below;
   __syncthreads();  // the plan area is reused below
+  BPC_STAMP(2, 3);
 
   // ---- b. selection: the kept candidates, in ascending key order, go to
   // the slice's range [off, off + kept) of the index list
@@ -884,6 +950,7 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(G 
   }
   kept = min(kept, k - off);
   __syncthreads();  // the list is complete and visible to the whole workgroup
+  BPC_STAMP(2, 4);
 
   // ---- c. attention: wavefront wid takes rows [16 (wid + 4 i), 16 (wid + 4 i) + 16)
   const char* Kh = reinterpret_cast<const char*>(K + b * sK_b + h * sK_h);
@@ -898,6 +965,9 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(G 
   }
   for (int r0 = wid * kAttnRows; r0 < kept; r0 += kAttnWaves * kAttnRows)
     attend_pass<G>(rows + r0, min(kAttnRows, kept - r0), sh.q, Kh, kstride, Vh, vstride, scale_log2, Mx, Ls, o);
+  BPC_STAMP(2, 5);
+  BPC_NOTE(2, 12, kept);
+  BPC_NOTE(2, 13, ncand);
 
   // ---- the slice's partial: each wavefront reduces o over its four row
   // groups; the wavefronts are combined under their common maximum
@@ -940,6 +1010,7 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(G 
     }
     pb[e] = acc;
   }
+  BPC_STAMP(2, 6);
 }
 
 // ---------------------------------------------------------------------------
@@ -959,6 +1030,7 @@ __global__ __launch_bounds__(kHeadDim) void merge_kernel(int Hkv, int G, int nch
   const size_t bh = (size_t)b * Hkv + h;
   const size_t cstride = (size_t)G * (kHeadDim + 2);
   const float* pg = part + bh * nchunks * cstride + (size_t)g * (kHeadDim + 2);
+  BPC_STAMP(3, 0);
   __shared__ float m_s[CB], l_s[CB];
   __shared__ float mx_s[2];
   // global maximum: the partial maxima are loaded in parallel
@@ -986,6 +1058,7 @@ __global__ __launch_bounds__(kHeadDim) void merge_kernel(int Hkv, int G, int nch
     __syncthreads();
   }
   out[(size_t)bq * kHeadDim + threadIdx.x] = acc / lsum;
+  BPC_STAMP(3, 1);
 }
 
 // ---------------------------------------------------------------------------
@@ -1040,6 +1113,12 @@ static hipError_t launch_decode_L(const DecodeArgs& a, const DecodeLayout& lay) 
   mark(4);
   return hipGetLastError();
 }
+
+#ifdef BPC_TRACE
+extern "C" int bpc_trace_buffer(void* buf) {
+  return hipMemcpyToSymbol(HIP_SYMBOL(g_trace), &buf, sizeof(buf)) == hipSuccess ? 0 : -1;
+}
+#endif
 
 hipError_t launch_decode(const DecodeArgs& a) {
   const DecodeLayout lay = decode_layout(a.B, a.Hq, a.Hkv, a.N, a.L, a.k);
