@@ -88,6 +88,7 @@ DecodeLayout decode_layout(int B, int Hq, int Hkv, int N, int L, int k) {
   d.off_meta = take(S * 4 * sizeof(uint32_t));
   d.off_hist_fine = take(S * (size_t)fine_stride(L) * sizeof(uint32_t));
   d.off_hist_cc = take(S * (size_t)kCoarseStride * sizeof(uint32_t));
+  d.off_win = take(S * (size_t)kWinRec * sizeof(uint32_t));
   d.off_part = take(S * d.G * (kHeadDim + 2) * sizeof(float));
   d.off_idx = take(BH * (size_t)k * sizeof(int32_t));
   d.off_qcode = take(BH * kQcodeStride * sizeof(uint32_t));

@@ -25,7 +25,7 @@ constexpr int kMaxSlices = 1024;
 // One attention workgroup per slice keeps its selected candidates, read in
 // batches of kCandBatch, and gathers their rows with four wavefronts.
 constexpr int kAttnThreads = 256;
-constexpr int kCandBatch = 4096;
+constexpr int kCandBatch = 1024;
 constexpr int kCoarseShift = 7;  // coarse histogram bin = distance >> 7
 constexpr int kCoarseBins = 128;
 constexpr int kMaxGroup = 16;  // query heads per KV head
@@ -38,6 +38,15 @@ __host__ __device__ constexpr int dist_bins(int L) { return 127 * L + 1; }
 // stride kCoarseStride.
 __host__ __device__ constexpr int fine_stride(int L) { return (dist_bins(L) + 3) & ~3; }
 constexpr int kCoarseStride = 132;
+// Per-slice window record: header [4] u32 (base, cand_max, keys with
+// distance < base, keys in the slice), then kWinBins cumulative counts (keys
+// with distance <= base + j) as u16 pairs.  The window ends a few standard
+// deviations above the slice's own estimate of the threshold (its
+// ceil(k cnt / N)-th smallest distance), and cand_max <= base + kWinBins - 1
+// is the largest distance on the slice's candidate list.
+constexpr int kWinBins = 128;
+constexpr int kWinRec = 4 + kWinBins / 2;  // u32 per record
+constexpr int kWinSlices = 64;             // slices per (b, h) the one-round threshold handles
 
 // ---- build tiling ----------------------------------------------------------
 constexpr int kBuildRows = 256;  // rows per workgroup in the build passes
@@ -45,15 +54,16 @@ constexpr int kBuildRows = 256;  // rows per workgroup in the build passes
 // ---- workspace layouts -----------------------------------------------------
 // Decode, per slice sl = (b Hkv + h) nslices + s: candidates [kSlice] u32
 // (key-in-slice << 16 | distance), meta [4] u32 (kth_s, lowest occupied
-// coarse bin, candidate count), fine histogram [fine_stride] u32, coarse
-// prefix [kCoarseStride] u32 and G partials of (max, sum, o[128]) fp32; per
-// (b, h) the packed query (8 W plane words, then sum |p|; stride
-// kQcodeStride) and the k selected indices (used when the caller passes no
-// idx_out).
+// coarse bin, candidate count, largest candidate distance), fine histogram
+// [fine_stride] u32, coarse
+// prefix [kCoarseStride] u32, window record [kWinRec] u32 and G partials of
+// (max, sum, o[128]) fp32; per (b, h) the packed query (8 W plane words,
+// then sum |p|; stride kQcodeStride) and the k selected indices (used when
+// the caller passes no idx_out and a slice keeps more rows than LDS holds).
 constexpr int kQcodeStride = 64;
 struct DecodeLayout {
   int nslices, G, W;
-  size_t off_cand, off_meta, off_hist_fine, off_hist_cc, off_part, off_idx, off_qcode, total;
+  size_t off_cand, off_meta, off_hist_fine, off_hist_cc, off_win, off_part, off_idx, off_qcode, total;
 };
 
 struct BuildLayout {

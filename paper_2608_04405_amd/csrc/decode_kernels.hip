@@ -311,7 +311,7 @@ struct ScoreShared {
   uint32_t coarse[kCoarseBins];
   uint32_t cc[kCoarseBins + 1];
   int cnt[128];
-  int cs, kth, cmin, total;
+  int cs, kth, cmin, total, cs2, that;
 };
 
 // FULL: the slice holds kSlice keys and its codes are 16-byte aligned, so no
@@ -321,7 +321,8 @@ __device__ __forceinline__ void score_body(ScoreShared<L>& sh, int bh, int s, co
                                            const uint32_t* __restrict__ codes, int64_t sC_b, int64_t sC_h, int Hkv,
                                            int N, int k, int nslices, uint32_t* __restrict__ cand,
                                            uint32_t* __restrict__ meta, uint32_t* __restrict__ hist_fine,
-                                           uint32_t* __restrict__ hist_cc, int32_t* __restrict__ score_out) {
+                                           uint32_t* __restrict__ hist_cc, uint32_t* __restrict__ win,
+                                           int32_t* __restrict__ score_out) {
   constexpr int W = L / 32;
   constexpr int NB = ScoreShared<L>::NB;
   constexpr int NBP = ScoreShared<L>::NBP;
@@ -450,8 +451,10 @@ __device__ __forceinline__ void score_body(ScoreShared<L>& sh, int bh, int s, co
   __syncthreads();
 
   BPC_STAMP(1, 2);
-  // wave 0: coarse prefix, the lowest occupied coarse bin, and the coarse bin
-  // holding the slice's k-th key
+  // wave 0: coarse prefix, the lowest occupied coarse bin, and the coarse
+  // bins holding the slice's k-th key and its m-th key, m = ceil(k cnt / N)
+  // (the slice's share of the budget: its own estimate of the threshold)
+  const int mloc = (int)(((int64_t)k * cnt + N - 1) / N);
   if (threadIdx.x < 64) {
     const uint32_t c0 = sh.coarse[2 * lane], c1 = sh.coarse[2 * lane + 1];
     int x = (int)(c0 + c1);
@@ -468,26 +471,53 @@ __device__ __forceinline__ void score_body(ScoreShared<L>& sh, int bh, int s, co
     const unsigned long long m1 = __ballot(x >= k);
     const int f0 = first_lane(m0), f1 = first_lane(m1);
     const int cs = min(f0 < 64 ? 2 * f0 : 1 << 30, f1 < 64 ? 2 * f1 + 1 : 1 << 30);
+    const unsigned long long n0m = __ballot(ex + (int)c0 >= mloc);
+    const unsigned long long n1m = __ballot(x >= mloc);
+    const int h0 = first_lane(n0m), h1 = first_lane(n1m);
+    const int cs2 = min(h0 < 64 ? 2 * h0 : 1 << 30, h1 < 64 ? 2 * h1 + 1 : 1 << 30);
     const unsigned long long z0 = __ballot(c0 != 0u), z1 = __ballot(c1 != 0u);
     const int g0 = first_lane(z0), g1 = first_lane(z1);
     if (lane == 0) {
       sh.cs = (cnt >= k) ? cs : -1;
+      sh.cs2 = cs2;  // mloc <= cnt: always found
       sh.kth = NB - 1;
+      sh.that = NB - 1;
       sh.cmin = min(g0 < 64 ? 2 * g0 : kCoarseBins - 1, g1 < 64 ? 2 * g1 + 1 : kCoarseBins - 1);
     }
   }
   __syncthreads();
-  if (threadIdx.x < (1 << kCoarseShift)) {
-    // the first fine bin of coarse bin cs where the count reaches k
-    const int cs = sh.cs;
-    const int t = (max(cs, 0) << kCoarseShift) + threadIdx.x;
+  if (threadIdx.x < 2 << kCoarseShift) {
+    // the first fine bin of coarse bin cs (threads 0..127) where the count
+    // reaches k, and of cs2 (threads 128..255) where it reaches mloc
+    const bool second = threadIdx.x >= (1 << kCoarseShift);
+    const int cs = second ? sh.cs2 : sh.cs, need = second ? mloc : k;
+    const int t = (max(cs, 0) << kCoarseShift) + (threadIdx.x & ((1 << kCoarseShift) - 1));
     const uint32_t v = (t < NBP) ? sh.u.hist[t] : 0u;
-    const unsigned long long m = __ballot(cs >= 0 && (int)sh.cc[max(cs, 0)] + (int)(v >> 16) + (int)(v & 0xFFFFu) >= k);
-    if (m && lane == first_lane(m)) atomicMin(&sh.kth, t);
+    const unsigned long long m = __ballot(cs >= 0 && (int)sh.cc[max(cs, 0)] + (int)(v >> 16) + (int)(v & 0xFFFFu) >= need);
+    if (m && lane == first_lane(m)) atomicMin(second ? &sh.that : &sh.kth, t);
   }
   __syncthreads();
   const int kth = sh.kth;
   const int cmin = sh.cmin;
+  // The window: kWinBins distances ending `up` above the slice's estimate
+  // t = sh.that, with `up` about six standard deviations of that estimate
+  // (sqrt(mloc) keys over the local density of keys per distance), and the
+  // largest distance a candidate may have, cand_max = min(t + up, kth); the
+  // one-round threshold is only accepted at or below every slice's cand_max.
+  int wbase, cand_max;
+  {
+    auto cumd = [&](int t) -> int {  // keys with distance <= t
+      if (t < 0) return 0;
+      if (t >= NBP) return cnt;
+      const uint32_t v = sh.u.hist[t];
+      return (int)(sh.cc[t >> kCoarseShift] + (v >> 16) + (v & 0xFFFFu));
+    };
+    const int that = sh.that;
+    const int dens17 = max(cumd(that + 8) - cumd(that - 9), 1);  // keys in 17 distances around t
+    const int up = min(max((int)ceilf(6.0f * sqrtf((float)mloc) * 17.0f / (float)dens17), 4), kWinBins - 32);
+    wbase = max(that + up - (kWinBins - 1), 0);
+    cand_max = min(that + up, kth);
+  }
   BPC_STAMP(1, 3);
 
   // ---- histograms for the threshold: coarse prefix (129 entries) and the
@@ -499,8 +529,23 @@ __device__ __forceinline__ void score_body(ScoreShared<L>& sh, int bh, int s, co
     uint32_t* hf = hist_fine + sl * FS;
     for (int t = (cmin << kCoarseShift) + threadIdx.x; t <= kth; t += NT) hf[t] = sh.u.hist[t];
   }
+  // ---- window record: cumulative counts over [wbase, wbase + kWinBins) as
+  // u16 pairs (the histogram is in prefix form over all of [0, NBP))
+  {
+    uint32_t* wr = win + sl * kWinRec;
+    auto cum = [&](int t) -> uint32_t {  // keys with distance <= t
+      if (t >= NBP) return (uint32_t)cnt;
+      const uint32_t v = sh.u.hist[t];
+      return sh.cc[t >> kCoarseShift] + (v >> 16) + (v & 0xFFFFu);
+    };
+    if (threadIdx.x < kWinBins / 2)
+      wr[4 + threadIdx.x] = cum(wbase + 2 * threadIdx.x) | (cum(wbase + 2 * threadIdx.x + 1) << 16);
+    else if (threadIdx.x == kWinBins / 2)
+      *reinterpret_cast<uint4*>(wr) =
+          make_uint4((uint32_t)wbase, (uint32_t)cand_max, wbase > 0 ? cum(wbase - 1) : 0u, (uint32_t)cnt);
+  }
 
-  // ---- candidates (dist <= kth) in key order, which is (wavefront, it,
+  // ---- candidates (dist <= cand_max) in key order, which is (wavefront, it,
   // lane, u): the wavefronts' counts are scanned once, then each wavefront
   // writes its candidates from a running offset
   {
@@ -508,7 +553,7 @@ __device__ __forceinline__ void score_body(ScoreShared<L>& sh, int bh, int s, co
 #pragma unroll
     for (int it = 0; it < NLD; ++it)
 #pragma unroll
-      for (int u = 0; u < KPL; ++u) c += is_cand(it, u, kth) ? 1 : 0;
+      for (int u = 0; u < KPL; ++u) c += is_cand(it, u, cand_max) ? 1 : 0;
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) c += __shfl_xor(c, o, 64);
     if (lane == 0) sh.cnt[wid] = c;
@@ -538,7 +583,7 @@ __device__ __forceinline__ void score_body(ScoreShared<L>& sh, int bh, int s, co
       bool f[KPL];
 #pragma unroll
       for (int u = 0; u < KPL; ++u) {
-        f[u] = is_cand(it, u, kth);
+        f[u] = is_cand(it, u, cand_max);
         const unsigned long long m = __ballot(f[u]);
         pos += (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
         base += (int)__popcll(m);
@@ -548,7 +593,7 @@ __device__ __forceinline__ void score_body(ScoreShared<L>& sh, int bh, int s, co
         if (f[u]) cs_out[pos++] = ((uint32_t)key_of(it, u) << 16) | (uint32_t)dist_of(it, u);
     }
   }
-  if (threadIdx.x == 0) *reinterpret_cast<uint4*>(meta + sl * 4) = make_uint4(kth, cmin, sh.total, 0u);
+  if (threadIdx.x == 0) *reinterpret_cast<uint4*>(meta + sl * 4) = make_uint4(kth, cmin, sh.total, cand_max);
   if (score_out) {  // debug output
     const int T = (int)qc[8 * W];
     int32_t* so = score_out + (size_t)bh * N + n0;
@@ -572,7 +617,8 @@ template <int L, bool FULL>
 __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(L <= 64 ? 8 : 4))) void score_kernel(
     const uint32_t* __restrict__ qcode_ws, const uint32_t* __restrict__ codes, int64_t sC_b, int64_t sC_h, int BH,
     int Hkv, int N, int k, int nslices, uint32_t* __restrict__ cand, uint32_t* __restrict__ meta,
-    uint32_t* __restrict__ hist_fine, uint32_t* __restrict__ hist_cc, int32_t* __restrict__ score_out) {
+    uint32_t* __restrict__ hist_fine, uint32_t* __restrict__ hist_cc, uint32_t* __restrict__ win,
+    int32_t* __restrict__ score_out) {
   __shared__ ScoreShared<L> sh;
   int bh, s;
   slice_tile(blockIdx.x, BH, nslices, bh, s);
@@ -581,7 +627,7 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(L
   if (full != FULL) return;
   BPC_STAMP(1, 0);
   score_body<L, FULL>(sh, bh, s, qcode_ws, codes, sC_b, sC_h, Hkv, N, k, nslices, cand, meta, hist_fine, hist_cc,
-                      score_out);
+                      win, score_out);
   BPC_STAMP(1, 4);
 }
 
@@ -638,9 +684,11 @@ constexpr int kAttnSlots = 4;                // rows per lane per pass
 constexpr int kAttnRows = 4 * kAttnSlots;    // rows per wavefront per pass
 constexpr int kPlanCache = 16;               // slices whose histograms are kept in LDS
 constexpr int kRoundBatch = 8;               // histogram loads per thread issued together
+constexpr int kRowCache = 2048;              // selected rows kept in LDS (more go through global memory)
 
 template <int G>
 struct AttendShared {
+  // two-round threshold (any slice count)
   struct Plan {
     int part[2][kCoarseBins], part2[2][kCoarseBins];
     int gp[kCoarseBins];
@@ -650,25 +698,28 @@ struct AttendShared {
   };
   union U {
     Plan plan;
-    float o[kAttnWaves][G][kHeadDim];
+    uint32_t win[kWinSlices][kWinRec];  // one-round threshold: the window records of the slices
+    int rows[kRowCache];                // the slice's selected keys, ascending
+    float o[kAttnWaves][G][kHeadDim];   // per-wavefront weighted V
   } u;
   float st[kAttnWaves][G][2];  // per wavefront (max, sum)
   uint4 q[G][kHeadDim / 8];     // the group's queries, bf16
   int wave_tot[kAttnWaves];
   int first[2];
   int red[2][kAttnWaves];
+  int plan3[3];  // one-round threshold: take, off, kept of this slice
 };
 
-// One pass of a wavefront over nrows (1..kAttnRows) rows rows[0..nrows):
-// updates its running maximum Mx and sum Ls (uniform over the wavefront) and
-// this lane's weighted-V partials o.
+// One pass of a wavefront over nrows (1..kAttnRows) rows; lane l < nrows
+// holds the key index of row l in myidx.  Updates the wavefront's running
+// maximum Mx and sum Ls (uniform over the wavefront) and this lane's
+// weighted-V partials o.
 template <int G>
-__device__ __forceinline__ void attend_pass(const int* rows, int nrows, const uint4 (*qs)[kHeadDim / 8], const char* Kh,
+__device__ __forceinline__ void attend_pass(int myidx, int nrows, const uint4 (*qs)[kHeadDim / 8], const char* Kh,
                                             uint32_t kstride, const char* Vh, uint32_t vstride, float scale_log2,
                                             float (&Mx)[G], float (&Ls)[G], float (&o)[G][8]) {
   const int lane = threadIdx.x & 63;
   const int l16 = lane & 15, rsub = lane >> 4;
-  const int myidx = (lane < nrows) ? rows[lane] : 0;
   bool ok[kAttnSlots];
   uint32_t rown[kAttnSlots];
 #pragma unroll
@@ -741,11 +792,12 @@ __device__ __forceinline__ void attend_pass(const int* rows, int nrows, const ui
 
 template <int G>
 __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(G <= 4 ? 4 : 1))) void attend_kernel(
-    int N, int k, int L, int BH, int Hkv, int nslices, const uint32_t* __restrict__ cand,
+    int N, int k, int L, int BH, int Hkv, int nslices, int win_ok, const uint32_t* __restrict__ cand,
     const uint32_t* __restrict__ meta, const uint32_t* __restrict__ hist_fine, const uint32_t* __restrict__ hist_cc,
-    int32_t* __restrict__ idx, const uint16_t* __restrict__ q, const uint16_t* __restrict__ K, int64_t sK_b,
-    int64_t sK_h, int64_t sK_n, const uint16_t* __restrict__ V, int64_t sV_b, int64_t sV_h, int64_t sV_n,
-    float scale_log2, float* __restrict__ part) {
+    const uint32_t* __restrict__ win, const uint32_t* __restrict__ codes, int64_t sC_b, int64_t sC_h,
+    const uint32_t* __restrict__ qcode, int32_t* __restrict__ idx, int write_idx, const uint16_t* __restrict__ q,
+    const uint16_t* __restrict__ K, int64_t sK_b, int64_t sK_h, int64_t sK_n, const uint16_t* __restrict__ V,
+    int64_t sV_b, int64_t sV_h, int64_t sV_n, float scale_log2, float* __restrict__ part) {
   constexpr int PER = kCandBatch / kAttnThreads;  // candidates per thread per batch
   __shared__ AttendShared<G> sh;
   typename AttendShared<G>::Plan& pl = sh.u.plan;
@@ -763,165 +815,287 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(G 
   const uint32_t* mtb = meta + (size_t)bh * nslices * 4;
   BPC_STAMP(2, 0);
 
-  // the candidate count and the first batch of candidates load while the
-  // threshold is derived (the candidate region always holds kSlice entries)
-  int ncand;
-  uint32_t cv[PER];
-  auto load_batch = [&](int base) {
-    const uint4* v = reinterpret_cast<const uint4*>(cs + base + threadIdx.x * PER);
-#pragma unroll
-    for (int r = 0; r < PER / 4; ++r) {
-      const uint4 x = v[r];
-      cv[4 * r] = x.x, cv[4 * r + 1] = x.y, cv[4 * r + 2] = x.z, cv[4 * r + 3] = x.w;
+  // ---- a. threshold: T*, the number `take` of this slice's keys at T* that
+  // are selected, this slice's offset `off` in the (b, h) index list and the
+  // number `kept` of keys it selects
+  int tstar = 0, take = 0, off = 0, kept = 0, ncand = 0;
+  bool planned = false;
+  uint32_t cv[PER];  // this thread's current batch of (key << 16 | distance) entries
+  auto load_cand = [&](int base) {  // a batch of the slice's candidate list
+    const uint4 x = *reinterpret_cast<const uint4*>(cs + base + threadIdx.x * PER);
+    cv[0] = x.x, cv[1] = x.y, cv[2] = x.z, cv[3] = x.w;
+  };
+  static_assert(PER == 4, "one 16-byte load of candidates per thread and batch");
+  auto load_queries = [&]() {  // the group's queries, staged in LDS
+    if (threadIdx.x < G * kHeadDim / 8) {
+      const uint4* qb = reinterpret_cast<const uint4*>(q + ((size_t)b * Hkv * G + (size_t)h * G) * kHeadDim);
+      sh.q[threadIdx.x / (kHeadDim / 8)][threadIdx.x % (kHeadDim / 8)] = qb[threadIdx.x];
     }
   };
-
-  // ---- a. threshold.  Round 1: GP(c + 1) = keys of all slices with coarse bin <= c
-  // (its loads go first; the candidates and the queries load behind them)
-  // Each round's loads are issued together: kRoundBatch slices per thread
-  // at a time, the slice index clamped so every load is unconditional, and
-  // entries past the last slice dropped after the load.
-  {
-    const int c = threadIdx.x & (kCoarseBins - 1), grp = threadIdx.x >> 7;
-    int acc = 0;
-    for (int u0 = grp; u0 < nslices; u0 += 2 * kRoundBatch) {
-      uint32_t v[kRoundBatch];
+  if (win_ok) {
+    // One round: the window records of every slice of (b, h) (at most
+    // kWinSlices).  Every window covers [lo - 1, hi] with lo = max_s base_s
+    // and hi = min_s cand_max_s <= min_s (base_s + kWinBins - 1).  When
+    // S(lo - 1) < k <= S(hi), with S(t) = sum_s cum_s(t), T* = lo +
+    // #{t in [lo, hi] : S(t) < k} <= hi, so every slice's candidate list
+    // holds all of its keys with distance <= T*; otherwise the two-round
+    // path runs.
+    constexpr int RV = (kWinSlices * kWinRec / 4 + kAttnThreads - 1) / kAttnThreads;
+    const int nv = nslices * (kWinRec / 4);
+    const uint4* wsrc = reinterpret_cast<const uint4*>(win + (size_t)bh * nslices * kWinRec);
+    uint4 wv[RV];
 #pragma unroll
-      for (int j = 0; j < kRoundBatch; ++j)
-        v[j] = ccb[(size_t)min(u0 + 2 * j, nslices - 1) * kCoarseStride + c + 1];
+    for (int r = 0; r < RV; ++r)
+      if (r * kAttnThreads < nv) wv[r] = wsrc[min((int)threadIdx.x + r * kAttnThreads, nv - 1)];
+    const uint4 mym = *reinterpret_cast<const uint4*>(mtb + s * 4);
+    load_cand(0);
+    load_queries();
+    uint4* wdst = reinterpret_cast<uint4*>(&sh.u.win[0][0]);
 #pragma unroll
-      for (int j = 0; j < kRoundBatch; ++j) {
-        const int u = u0 + 2 * j;
-        if (u < nslices) {
-          acc += (int)v[j];
-          if (cached) pl.cc[u][c + 1] = v[j];
+    for (int r = 0; r < RV; ++r)
+      if ((int)threadIdx.x + r * kAttnThreads < nv) wdst[threadIdx.x + r * kAttnThreads] = wv[r];
+    ncand = min((int)mym.z, kSlice);
+    __syncthreads();
+    auto cum = [&](int u, int t) -> int {  // base_u - 1 <= t < base_u + kWinBins
+      const int j = t - (int)sh.u.win[u][0];
+      const uint32_t w = sh.u.win[u][4 + (max(j, 0) >> 1)];
+      return (j < 0) ? (int)sh.u.win[u][2] : (int)((j & 1) ? (w >> 16) : (w & 0xFFFFu));
+    };
+    int lo = 0, hi = 1 << 30;
+    for (int u = 0; u < nslices; ++u) lo = max(lo, (int)sh.u.win[u][0]), hi = min(hi, (int)sh.u.win[u][1]);
+    int below = 0, bad = lo > hi;
+    const int t = lo - 1 + (int)threadIdx.x;  // hi - lo + 2 <= kWinBins + 1 <= kAttnThreads values
+    if (!bad && t <= hi) {
+      int St = 0;
+      for (int u = 0; u < nslices; ++u) St += cum(u, t);
+      if (t == lo - 1)
+        bad = St >= k;
+      else
+        below = St < k;
+      if (t == hi && St < k) bad = 1;
+    }
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) below += __shfl_xor(below, o, 64), bad |= __shfl_xor(bad, o, 64);
+    if (lane == 0) sh.red[0][wid] = below, sh.red[1][wid] = bad;
+    __syncthreads();
+    int cntlow = 0;
+    bad = 0;
+#pragma unroll
+    for (int w = 0; w < kAttnWaves; ++w) cntlow += sh.red[0][w], bad |= sh.red[1][w];
+    if (!bad) {
+      tstar = lo + cntlow;
+      // keys below T* and ties at T*, per slice (wavefront 0, lane u = slice
+      // u); ties go to the lowest indices, i.e. slice by slice
+      if (wid == 0) {
+        int bu = 0, tu = 0;
+        if (lane < nslices) {
+          bu = cum(lane, tstar - 1);
+          tu = cum(lane, tstar) - bu;
+        }
+        int bi = bu, ti = tu;  // inclusive prefix over slices
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+          const int yb = __shfl_up(bi, o, 64), yt = __shfl_up(ti, o, 64);
+          if (lane >= o) bi += yb, ti += yt;
+        }
+        const int below_all = __shfl(bi, 63, 64);
+        if (lane == s) {
+          const int need = k - below_all;  // keys at T* to take, over all slices
+          const int below_before = bi - bu, ties_before = ti - tu;
+          const int tk = max(0, min(tu, need - ties_before));
+          sh.plan3[0] = tk;
+          sh.plan3[1] = below_before + min(need, ties_before);
+          sh.plan3[2] = bu + tk;
         }
       }
+      __syncthreads();
+      take = sh.plan3[0], off = sh.plan3[1], kept = sh.plan3[2];
+      planned = true;
     }
-    pl.part[grp][c] = acc;
-    if (cached && threadIdx.x < nslices) {
-      const uint4 m = *reinterpret_cast<const uint4*>(mtb + threadIdx.x * 4);
-      pl.cc[threadIdx.x][0] = 0u;
-      pl.kth[threadIdx.x] = min((int)m.x, NB - 1);
-      pl.cmin[threadIdx.x] = min((int)m.y, kCoarseBins - 1);
-    }
+    __syncthreads();  // the window area is reused below
   }
-  ncand = min((int)mtb[s * 4 + 2], kSlice);
-  load_batch(0);
-  if (threadIdx.x < G * kHeadDim / 8) {  // the group's queries, staged in LDS
-    const uint4* qb = reinterpret_cast<const uint4*>(q + ((size_t)b * Hkv * G + (size_t)h * G) * kHeadDim);
-    sh.q[threadIdx.x / (kHeadDim / 8)][threadIdx.x % (kHeadDim / 8)] = qb[threadIdx.x];
-  }
-  __syncthreads();
-  if (threadIdx.x < kCoarseBins) {
-    const int acc = pl.part[0][threadIdx.x] + pl.part[1][threadIdx.x];
-    pl.gp[threadIdx.x] = acc;
-    const unsigned long long m = __ballot(acc >= k);
-    if (lane == 0) sh.first[wid] = m ? first_lane(m) + 64 * wid : (1 << 30);
-  }
-  __syncthreads();
-  const int cstar = min(min(sh.first[0], sh.first[1]), kCoarseBins - 1);
-  BPC_STAMP(2, 1);
-  const int below_c = (cstar > 0) ? pl.gp[cstar - 1] : 0;  // keys with coarse bin < c*
-  __syncthreads();
-  // Round 2: the fine bins of c*, summed over slices (bins a slice did not
-  // write are empty below its cmin and never needed above its kth)
-  {
-    const int j = threadIdx.x & ((1 << kCoarseShift) - 1), grp = threadIdx.x >> 7;
-    const int t = (cstar << kCoarseShift) + j;
-    const int tc = min(t, NB - 1);
-    int exc = 0, inc = 0;
-    for (int u0 = grp; u0 < nslices; u0 += 2 * kRoundBatch) {
-      int kthu[kRoundBatch], cminu[kRoundBatch];
-      uint32_t v[kRoundBatch];
+  if (!planned) {
+    // Two rounds.  Round 1: GP(c + 1) = keys of all slices with coarse bin
+    // <= c.  Each round's loads are issued together: kRoundBatch slices per
+    // thread at a time, the slice index clamped so every load is
+    // unconditional, and entries past the last slice dropped after the load.
+    {
+      const int c = threadIdx.x & (kCoarseBins - 1), grp = threadIdx.x >> 7;
+      int acc = 0;
+      for (int u0 = grp; u0 < nslices; u0 += 2 * kRoundBatch) {
+        uint32_t v[kRoundBatch];
 #pragma unroll
-      for (int i = 0; i < kRoundBatch; ++i) {
-        const int u = min(u0 + 2 * i, nslices - 1);
-        if (cached) {
-          kthu[i] = pl.kth[u], cminu[i] = pl.cmin[u];
-        } else {
-          const uint2 m = *reinterpret_cast<const uint2*>(mtb + u * 4);
-          kthu[i] = (int)m.x, cminu[i] = (int)m.y;
-        }
-        v[i] = hfb[(size_t)u * FS + tc];  // a bin the slice did not write is dropped below
-      }
+        for (int j = 0; j < kRoundBatch; ++j)
+          v[j] = ccb[(size_t)min(u0 + 2 * j, nslices - 1) * kCoarseStride + c + 1];
 #pragma unroll
-      for (int i = 0; i < kRoundBatch; ++i) {
-        const int u = u0 + 2 * i;
-        if (u < nslices) {
-          const uint32_t x = (t < NB && t >= (cminu[i] << kCoarseShift) && t <= kthu[i]) ? v[i] : 0u;
-          if (cached) pl.fine[u][j] = x;
-          exc += (int)(x >> 16);
-          inc += (int)(x >> 16) + (int)(x & 0xFFFFu);
+        for (int j = 0; j < kRoundBatch; ++j) {
+          const int u = u0 + 2 * j;
+          if (u < nslices) {
+            acc += (int)v[j];
+            if (cached) pl.cc[u][c + 1] = v[j];
+          }
         }
       }
+      pl.part[grp][c] = acc;
+      if (cached && threadIdx.x < nslices) {
+        const uint4 m = *reinterpret_cast<const uint4*>(mtb + threadIdx.x * 4);
+        pl.cc[threadIdx.x][0] = 0u;
+        pl.kth[threadIdx.x] = min((int)m.x, NB - 1);
+        pl.cmin[threadIdx.x] = min((int)m.y, kCoarseBins - 1);
+      }
     }
-    pl.part[grp][j] = exc;
-    pl.part2[grp][j] = inc;
-  }
-  __syncthreads();
-  if (threadIdx.x < (1 << kCoarseShift)) {
-    const int exc = pl.part[0][threadIdx.x] + pl.part[1][threadIdx.x];
-    const int inc = pl.part2[0][threadIdx.x] + pl.part2[1][threadIdx.x];
-    const int t = (cstar << kCoarseShift) + threadIdx.x;
-    const unsigned long long m = __ballot(t < NB && below_c + inc >= k);
-    if (lane == 0) sh.first[wid] = m ? first_lane(m) + 64 * wid : (1 << 30);
-    pl.gp[threadIdx.x] = exc;
-  }
-  __syncthreads();
-  const int jt = min(min(sh.first[0], sh.first[1]), (1 << kCoarseShift) - 1);
-  BPC_STAMP(2, 2);
-  const int tstar = min((cstar << kCoarseShift) + jt, NB - 1);
-  const int need = k - (below_c + pl.gp[jt]);  // keys at T* to take, over all slices
-  // Round 3: keys below T* and ties at T* of the slices before this one (and
-  // this slice's own ties).  The slices before s take min(need, their ties)
-  // of the ties; this slice takes what is left, up to its own.
-  auto slice_at_tstar = [&](int u, int& below, int& tie) {
-    uint32_t v;
-    int ccv;
-    if (cached) {
-      v = pl.fine[u][jt];
-      ccv = (int)pl.cc[u][cstar];
-    } else {
-      const int cminu = (int)mtb[u * 4 + 1];
-      v = (tstar >= (cminu << kCoarseShift)) ? hfb[(size_t)u * FS + tstar] : 0u;
-      ccv = (int)ccb[(size_t)u * kCoarseStride + cstar];
+    if (!win_ok) load_queries();  // else already staged
+    __syncthreads();
+    if (threadIdx.x < kCoarseBins) {
+      const int acc = pl.part[0][threadIdx.x] + pl.part[1][threadIdx.x];
+      pl.gp[threadIdx.x] = acc;
+      const unsigned long long m = __ballot(acc >= k);
+      if (lane == 0) sh.first[wid] = m ? first_lane(m) + 64 * wid : (1 << 30);
     }
-    below = ccv + (int)(v >> 16);
-    tie = (int)(v & 0xFFFFu);
-  };
-  int bl = 0, ti = 0;
-  for (int u = threadIdx.x; u < s; u += kAttnThreads) {
-    int bu, tu;
-    slice_at_tstar(u, bu, tu);
-    bl += bu, ti += tu;
-  }
+    __syncthreads();
+    const int cstar = min(min(sh.first[0], sh.first[1]), kCoarseBins - 1);
+    const int below_c = (cstar > 0) ? pl.gp[cstar - 1] : 0;  // keys with coarse bin < c*
+    __syncthreads();
+    // Round 2: the fine bins of c*, summed over slices (bins a slice did not
+    // write are empty below its cmin and never needed above its kth)
+    {
+      const int j = threadIdx.x & ((1 << kCoarseShift) - 1), grp = threadIdx.x >> 7;
+      const int t = (cstar << kCoarseShift) + j;
+      const int tc = min(t, NB - 1);
+      int exc = 0, inc = 0;
+      for (int u0 = grp; u0 < nslices; u0 += 2 * kRoundBatch) {
+        int kthu[kRoundBatch], cminu[kRoundBatch];
+        uint32_t v[kRoundBatch];
 #pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    bl += __shfl_xor(bl, o, 64);
-    ti += __shfl_xor(ti, o, 64);
-  }
-  if (lane == 0) sh.red[0][wid] = bl, sh.red[1][wid] = ti;
-  int my_below, my_tie;
-  slice_at_tstar(s, my_below, my_tie);
-  __syncthreads();
-  int below_before = 0, ties_before = 0;
+        for (int i = 0; i < kRoundBatch; ++i) {
+          const int u = min(u0 + 2 * i, nslices - 1);
+          if (cached) {
+            kthu[i] = pl.kth[u], cminu[i] = pl.cmin[u];
+          } else {
+            const uint2 m = *reinterpret_cast<const uint2*>(mtb + u * 4);
+            kthu[i] = (int)m.x, cminu[i] = (int)m.y;
+          }
+          v[i] = hfb[(size_t)u * FS + tc];  // a bin the slice did not write is dropped below
+        }
 #pragma unroll
-  for (int w = 0; w < kAttnWaves; ++w) below_before += sh.red[0][w], ties_before += sh.red[1][w];
-  const int take = max(0, min(my_tie, need - ties_before));
-  const int off = below_before + min(need, ties_before);
-  (void)my_below;
-  __syncthreads();  // the plan area is reused below
+        for (int i = 0; i < kRoundBatch; ++i) {
+          const int u = u0 + 2 * i;
+          if (u < nslices) {
+            const uint32_t x = (t < NB && t >= (cminu[i] << kCoarseShift) && t <= kthu[i]) ? v[i] : 0u;
+            if (cached) pl.fine[u][j] = x;
+            exc += (int)(x >> 16);
+            inc += (int)(x >> 16) + (int)(x & 0xFFFFu);
+          }
+        }
+      }
+      pl.part[grp][j] = exc;
+      pl.part2[grp][j] = inc;
+    }
+    __syncthreads();
+    if (threadIdx.x < (1 << kCoarseShift)) {
+      const int exc = pl.part[0][threadIdx.x] + pl.part[1][threadIdx.x];
+      const int inc = pl.part2[0][threadIdx.x] + pl.part2[1][threadIdx.x];
+      const int t = (cstar << kCoarseShift) + threadIdx.x;
+      const unsigned long long m = __ballot(t < NB && below_c + inc >= k);
+      if (lane == 0) sh.first[wid] = m ? first_lane(m) + 64 * wid : (1 << 30);
+      pl.gp[threadIdx.x] = exc;
+    }
+    __syncthreads();
+    const int jt = min(min(sh.first[0], sh.first[1]), (1 << kCoarseShift) - 1);
+    tstar = min((cstar << kCoarseShift) + jt, NB - 1);
+    const int need = k - (below_c + pl.gp[jt]);  // keys at T* to take, over all slices
+    // Round 3: keys below T* and ties at T* of the slices before this one
+    // (and this slice's own ties).  The slices before s take min(need, their
+    // ties) of the ties; this slice takes what is left, up to its own.
+    auto slice_at_tstar = [&](int u, int& below, int& tie) {
+      uint32_t v;
+      int ccv;
+      if (cached) {
+        v = pl.fine[u][jt];
+        ccv = (int)pl.cc[u][cstar];
+      } else {
+        const int cminu = (int)mtb[u * 4 + 1];
+        v = (tstar >= (cminu << kCoarseShift)) ? hfb[(size_t)u * FS + tstar] : 0u;
+        ccv = (int)ccb[(size_t)u * kCoarseStride + cstar];
+      }
+      below = ccv + (int)(v >> 16);
+      tie = (int)(v & 0xFFFFu);
+    };
+    int bl = 0, ti = 0;
+    for (int u = threadIdx.x; u < s; u += kAttnThreads) {
+      int bu, tu;
+      slice_at_tstar(u, bu, tu);
+      bl += bu, ti += tu;
+    }
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      bl += __shfl_xor(bl, o, 64);
+      ti += __shfl_xor(ti, o, 64);
+    }
+    if (lane == 0) sh.red[0][wid] = bl, sh.red[1][wid] = ti;
+    int my_below, my_tie;
+    slice_at_tstar(s, my_below, my_tie);
+    __syncthreads();
+    int below_before = 0, ties_before = 0;
+#pragma unroll
+    for (int w = 0; w < kAttnWaves; ++w) below_before += sh.red[0][w], ties_before += sh.red[1][w];
+    take = max(0, min(my_tie, need - ties_before));
+    off = below_before + min(need, ties_before);
+    kept = my_below + take;
+    __syncthreads();  // the plan area is reused below
+  }
+  kept = min(kept, k - off);
   BPC_STAMP(2, 3);
 
   // ---- b. selection: the kept candidates, in ascending key order, go to
-  // the slice's range [off, off + kept) of the index list
-  int32_t* rows = idx + (size_t)bh * k + off;
-  int kept = 0, tie_seen = 0;  // kept keys and ties at T* in earlier batches
-  for (int base = 0; base < ncand; base += kCandBatch) {
-    if (base > 0) load_batch(base);
-    // distances of this thread's candidates; entries past the count never match
-    const int nvalid = ncand - base - (int)threadIdx.x * PER;
+  // the slice's range [off, off + kept) of the index list: to the LDS row
+  // list when it holds them, and to global memory when it does not or when
+  // the caller asked for the indices
+  // In the one-round path the entries are the slice's candidate list (it
+  // holds every key with distance <= T* since T* <= hi <= cand_max_s);
+  // otherwise the slice's codes are scored again.
+  const bool rows_lds = kept <= kRowCache;
+  const bool rows_glb = !rows_lds || write_idx;
+  int32_t* grows = idx + (size_t)bh * k + off;
+  const int nent = planned ? ncand : min(kSlice, N - n0);
+  const int W = L / 32;
+  uint32_t sg[4] = {0u, 0u, 0u, 0u}, M[7][4] = {};
+  const uint32_t* cb = codes + b * sC_b + h * sC_h + (int64_t)n0 * W;
+  if (!planned) {
+    const uint32_t* qc = qcode + (size_t)bh * kQcodeStride;
+#pragma unroll
+    for (int w = 0; w < 4; ++w)
+      if (w < W) {
+        sg[w] = qc[w];
+#pragma unroll
+        for (int j = 0; j < 7; ++j) M[j][w] = qc[(1 + j) * W + w];
+      }
+  }
+  auto rescore = [&](int base) {  // entries of keys base + PER t + e, scored from their codes
+#pragma unroll
+    for (int e = 0; e < PER; ++e) {
+      const int key = base + (int)threadIdx.x * PER + e;
+      uint32_t d = 0;
+      if (key < nent) {
+#pragma unroll
+        for (int w = 0; w < 4; ++w)
+          if (w < W) {
+            const uint32_t x = cb[(int64_t)key * W + w] ^ sg[w];
+#pragma unroll
+            for (int j = 0; j < 7; ++j) d += (uint32_t)__popc(M[j][w] & x) << j;
+          }
+      }
+      cv[e] = ((uint32_t)key << 16) | d;
+    }
+  };
+  int nkept = 0, tie_seen = 0;  // kept keys and ties at T* in earlier batches
+  for (int base = 0; base < nent; base += kCandBatch) {
+    if (!planned)
+      rescore(base);
+    else if (base > 0)
+      load_cand(base);
+    // distances of this thread's entries; entries past the count never match
+    const int nvalid = nent - base - (int)threadIdx.x * PER;
     int nb = 0, nt = 0;
 #pragma unroll
     for (int e = 0; e < PER; ++e) {
@@ -933,7 +1107,7 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(G 
     // one scan of packed (ties << 16 | below): at most kCandBatch of each per batch
     const int pre = block_exclusive_scan<kAttnThreads>((nt << 16) | nb, sh.wave_tot, tot);
     int tie_rank = tie_seen + (pre >> 16);
-    int rank = kept + (pre & 0xFFFF) + max(0, min(tie_rank, take) - min(tie_seen, take));
+    int rank = nkept + (pre & 0xFFFF) + max(0, min(tie_rank, take) - min(tie_seen, take));
 #pragma unroll
     for (int e = 0; e < PER; ++e) {
       const int d = (e < nvalid) ? (int)(cv[e] & 0xFFFFu) : (1 << 30);
@@ -942,13 +1116,16 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(G 
         keep = tie_rank < take;
         ++tie_rank;
       }
-      if (keep && rank < k - off) rows[rank] = n0 + (int)(cv[e] >> 16);
+      if (keep && rank < kept) {
+        const int key = n0 + (int)(cv[e] >> 16);
+        if (rows_lds) sh.u.rows[rank] = key;
+        if (rows_glb) grows[rank] = key;
+      }
       rank += keep;
     }
-    kept += (tot & 0xFFFF) + max(0, min(tie_seen + (tot >> 16), take) - min(tie_seen, take));
+    nkept += (tot & 0xFFFF) + max(0, min(tie_seen + (tot >> 16), take) - min(tie_seen, take));
     tie_seen += tot >> 16;
   }
-  kept = min(kept, k - off);
   __syncthreads();  // the list is complete and visible to the whole workgroup
   BPC_STAMP(2, 4);
 
@@ -963,11 +1140,22 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(G 
 #pragma unroll
     for (int e = 0; e < 8; ++e) o[g][e] = 0.f;
   }
-  for (int r0 = wid * kAttnRows; r0 < kept; r0 += kAttnWaves * kAttnRows)
-    attend_pass<G>(rows + r0, min(kAttnRows, kept - r0), sh.q, Kh, kstride, Vh, vstride, scale_log2, Mx, Ls, o);
+  if (rows_lds) {
+    for (int r0 = wid * kAttnRows; r0 < kept; r0 += kAttnWaves * kAttnRows) {
+      const int nr = min(kAttnRows, kept - r0);
+      attend_pass<G>(lane < nr ? sh.u.rows[r0 + lane] : 0, nr, sh.q, Kh, kstride, Vh, vstride, scale_log2, Mx, Ls, o);
+    }
+  } else {
+    for (int r0 = wid * kAttnRows; r0 < kept; r0 += kAttnWaves * kAttnRows) {
+      const int nr = min(kAttnRows, kept - r0);
+      attend_pass<G>(lane < nr ? grows[r0 + lane] : 0, nr, sh.q, Kh, kstride, Vh, vstride, scale_log2, Mx, Ls, o);
+    }
+  }
   BPC_STAMP(2, 5);
   BPC_NOTE(2, 12, kept);
   BPC_NOTE(2, 13, ncand);
+  BPC_NOTE(2, 14, planned);
+  __syncthreads();  // the row list is read to the end before its area holds o
 
   // ---- the slice's partial: each wavefront reduces o over its four row
   // groups; the wavefronts are combined under their common maximum
@@ -1071,6 +1259,7 @@ static hipError_t launch_decode_L(const DecodeArgs& a, const DecodeLayout& lay) 
   uint32_t* meta = reinterpret_cast<uint32_t*>(a.ws + lay.off_meta);
   uint32_t* hist_fine = reinterpret_cast<uint32_t*>(a.ws + lay.off_hist_fine);
   uint32_t* hist_cc = reinterpret_cast<uint32_t*>(a.ws + lay.off_hist_cc);
+  uint32_t* win = reinterpret_cast<uint32_t*>(a.ws + lay.off_win);
   float* part = reinterpret_cast<float*>(a.ws + lay.off_part);
   int32_t* idx = a.idx_out ? a.idx_out : reinterpret_cast<int32_t*>(a.ws + lay.off_idx);
   uint32_t* qcode = reinterpret_cast<uint32_t*>(a.ws + lay.off_qcode);
@@ -1080,24 +1269,28 @@ static hipError_t launch_decode_L(const DecodeArgs& a, const DecodeLayout& lay) 
     if (a.events) (void)hipEventRecord(a.events[i], st);
   };
   const int nwg = BH * lay.nslices;
+  // the one-round threshold reads the window records of at most kWinSlices slices
+  const int win_ok = lay.nslices <= kWinSlices;
 
   mark(0);
   qpack_kernel<L><<<BH, kScanThreads, 0, st>>>(a.q, a.P, a.sP_b, a.sP_h, a.Hkv, lay.G, qcode, a.qcode_out);
   mark(1);
   score_kernel<L, true><<<nwg, kScoreThreads, 0, st>>>(qcode, a.codes, a.sC_b, a.sC_h, BH, a.Hkv, a.N, a.k,
-                                                     lay.nslices, cand, meta, hist_fine, hist_cc, a.score_out);
+                                                     lay.nslices, cand, meta, hist_fine, hist_cc, win, a.score_out);
   // slices of the other kind: a ragged last slice, or codes whose head or
   // batch stride is not a multiple of four words (the base is 16-byte aligned)
   if (a.N % kSlice != 0 || (a.sC_b * 4) % 16 != 0 || (a.sC_h * 4) % 16 != 0)
     score_kernel<L, false><<<nwg, kScoreThreads, 0, st>>>(qcode, a.codes, a.sC_b, a.sC_h, BH, a.Hkv, a.N, a.k,
-                                                          lay.nslices, cand, meta, hist_fine, hist_cc, a.score_out);
+                                                          lay.nslices, cand, meta, hist_fine, hist_cc, win, a.score_out);
   mark(2);
   switch (lay.G) {
 #define BPC_ATTEND_CASE(GG)                                                                                     \
   case GG:                                                                                                      \
-    attend_kernel<GG><<<nwg, kAttnThreads, 0, st>>>(a.N, a.k, L, BH, a.Hkv, lay.nslices, cand, meta, hist_fine, \
-                                                    hist_cc, idx, a.q, a.K, a.sK_b, a.sK_h, a.sK_n, a.V,  \
-                                                    a.sV_b, a.sV_h, a.sV_n, scale_log2, part);                 \
+    attend_kernel<GG><<<nwg, kAttnThreads, 0, st>>>(a.N, a.k, L, BH, a.Hkv, lay.nslices, win_ok, cand, meta,    \
+                                                    hist_fine, hist_cc, win, a.codes, a.sC_b, a.sC_h, qcode, idx, \
+                                                    a.idx_out != nullptr, a.q, a.K,                               \
+                                                    a.sK_b, a.sK_h, a.sK_n, a.V, a.sV_b, a.sV_h, a.sV_n,          \
+                                                    scale_log2, part);                                            \
     break;
     BPC_ATTEND_CASE(1)
     BPC_ATTEND_CASE(2)

@@ -291,6 +291,23 @@ def test_decode_edge_cases(case):
     _decode_and_compare(q, K, V, codes, P, case["k"], N=case["N"], label=f"edge {case}")
 
 
+def test_decode_threshold_below_the_windows():
+    """Two slices, each with 60 keys whose code equals the query's sign plane
+    (distance 0) and all other keys far away, k = 100: every slice's k-th
+    smallest distance is far above 0, so the threshold lies below the
+    per-slice windows the one-round threshold reads and the exact two-round
+    path must produce it (ties at distance 0 go to the lowest indices)."""
+    rng = np.random.default_rng(11)
+    N, L, k = 32768, 64, 100
+    announce(f"[decode window miss] N={N} L={L} k={k}")
+    q, K, V, codes, P = _random_case(rng, 1, 4, 1, N, L)
+    planes = oracle.quantize_query(bits(q)[0], P[0, 0])["qcode"]
+    near = np.r_[0:60, 16384:16444]
+    codes[0, 0, near] = planes[0]
+    _, idx = _decode_and_compare(q, K, V, codes, P, k, label="window miss")
+    assert np.array_equal(idx[0, 0].cpu().numpy(), near[:k])
+
+
 def test_decode_garbage_workspace():
     """The workspace needs no clearing: a first call on random bytes, and
     later calls on the same workspace, all match the oracle."""
