@@ -27,8 +27,8 @@ reproducible (the paper does not fix it):
   bit value 1 means h_i = +1.
 
 Parity status: every function below is pinned by the CPU tests (closed
-forms, exact rational re-evaluation, invariants, library routines); none is
-"parity unpinned".  The method-quality diagnostics (needle recall, cosine
+forms, exact rational re-evaluation, invariants, library routines, brute
+force); none is "parity unpinned".  The method-quality diagnostics (needle recall, cosine
 similarity with full attention) are reported, not part of parity.
 """
 
@@ -53,6 +53,9 @@ __all__ = [
     "full_attention",
     "exact_topk",
     "decode_head",
+    "select_hard",
+    "eas_budget",
+    "decode_head_eas",
     "budget_keys",
     "FRAGILE_THRESHOLD",
 ]
@@ -379,3 +382,53 @@ def decode_head(q_bits, K_bits, V_bits, codes, P, k: int, sm_scale: float):
     idx = select_topk(c, k)
     out = attend(q_bits, K_bits, V_bits, idx, sm_scale)
     return {"p": qq["p"], "qcode": qq["qcode"], "T": qq["T"], "scores": c, "idx": idx, "out": out}
+
+
+# --------------------------------------------------------------------------
+# Error-Aware Safeguard (Sec. 3.2 "Error-Aware Safeguard (EAS)", Eq.
+# reconstruction_error and Eq. safeguard_union; Sec. 4.1 "Baselines": 10 %
+# of the token budget is reserved for EAS)
+# --------------------------------------------------------------------------
+
+def eas_budget(budget: int, num: int = 1, den: int = 10) -> tuple[int, int]:
+    """Split a token budget into (k_hash, m): m = ceil(budget * num / den)
+    keys are reserved for the hard-to-hash set and k_hash = budget - m are
+    taken by hash score; m is capped at budget - 1 so that k_hash >= 1."""
+    if budget < 1:
+        raise ValueError("budget must be >= 1")
+    m = min(-(-budget * num // den), budget - 1)
+    return budget - m, m
+
+
+def select_hard(err, m: int) -> np.ndarray:
+    """The hard-to-hash set S_err: indices of the m largest reconstruction
+    errors ||k - h P|| (given as float32, the precision the library stores
+    them in), ordered by value with equal values going to the lower index.
+    Values are compared in the IEEE total order of float32.  Returned in
+    ascending index order (int64)."""
+    e = np.asarray(err, dtype=np.float32)
+    N = e.shape[0]
+    if not 0 <= m <= N:
+        raise ValueError("need 0 <= m <= N")
+    u = e.view(np.uint32).astype(np.int64)
+    key = np.where(u >= (1 << 31), (~u) & 0xFFFFFFFF, u | (1 << 31))  # total order, larger = larger
+    order = np.lexsort((np.arange(N), -key))
+    return np.sort(order[:m])
+
+
+def decode_head_eas(q_bits, K_bits, V_bits, codes, P, k_hash: int, serr, sm_scale: float):
+    """decode_head with the safeguard: attention over S_attn = S_hash u S_err,
+    S_hash the k_hash keys with the highest hash scores and S_err a given
+    index set (from select_hard at prefill).  Also returns, per entry of
+    S_err, whether it was added to S_hash (1) or already in it (0)."""
+    P = np.asarray(P, dtype=np.float32)
+    L = P.shape[0]
+    qq = quantize_query(q_bits, P)
+    c = hash_scores(codes, qq["p"], L)
+    idx = select_topk(c, k_hash)
+    serr = np.asarray(serr, dtype=np.int64)
+    added = (~np.isin(serr, idx)).astype(np.int32)
+    union = np.union1d(idx, serr)
+    out = attend(q_bits, K_bits, V_bits, union, sm_scale)
+    return {"p": qq["p"], "qcode": qq["qcode"], "scores": c, "idx": idx, "union": union, "added": added,
+            "out": out}

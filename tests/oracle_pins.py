@@ -499,4 +499,73 @@ def pin_topk_baseline(o):
     assert np.allclose(out, w @ bf16_values(V[expect]), rtol=1e-12, atol=1e-13)
 
 
+# ---------------------------------------------------------------- error-aware safeguard
+
+def pin_eas_budget(o):
+    # 10 % of the budget is reserved for the safeguard (Sec. 4.1), rounded up
+    # like the budget itself; k_hash keeps at least one key
+    assert o.eas_budget(2622) == (2359, 263)   # 2 % of 131072 keys
+    assert o.eas_budget(10) == (9, 1)
+    assert o.eas_budget(11) == (9, 2)
+    assert o.eas_budget(2) == (1, 1)
+    assert o.eas_budget(1) == (1, 0)
+    assert o.eas_budget(100, 15, 100) == (85, 15)
+
+
+def pin_select_hard(o):
+    rng = np.random.default_rng(26)
+    for N, m in ((40, 5), (300, 300), (257, 1), (1000, 37)):
+        e = rng.choice(np.array([0.0, 0.5, 1.25, 3.0, 7.5], np.float32), size=N)  # many ties
+        expect = sorted(sorted(range(N), key=lambda j: (-float(e[j]), j))[:m])
+        assert o.select_hard(e, m).tolist() == expect
+    assert o.select_hard(np.ones(5, np.float32), 0).tolist() == []
+    # IEEE total order: -0 below +0, negatives below both
+    assert o.select_hard(np.array([0.0, -0.0], np.float32), 1).tolist() == [0]
+    assert o.select_hard(np.array([-0.0, 0.0], np.float32), 1).tolist() == [1]
+    assert o.select_hard(np.array([-1.0, -0.0, -2.0], np.float32), 2).tolist() == [0, 1]
+    # a key far outside the subspace of the others is the hardest to hash
+    # (the "passkey" situation the safeguard is for, Sec. 4.3)
+    N, D, L = 200, 128, 32
+    Kv = bf16_values(_lowrank_keys(rng, N, D))
+    out = np.zeros(D)
+    out[7] = 3.0 * np.linalg.norm(Kv, axis=1).max()  # off the keys' 4-dimensional subspace
+    Kv[113] = out
+    Kb = to_bf16_bits(Kv)
+    G = rng.standard_normal((L, D)).astype(np.float32)
+    _, _, err, _ = o.build_binary_pcs(Kb, G)
+    assert o.select_hard(err.astype(np.float32), 1).tolist() == [113]
+
+
+def pin_eas_union(o):
+    rng = np.random.default_rng(27)
+    N, D, Gq, L, k = 500, 128, 2, 64, 20
+    q = random_bf16(rng, (Gq, D))
+    K = random_bf16(rng, (N, D))
+    V = random_bf16(rng, (N, D))
+    codes = rng.integers(0, 1 << 32, size=(N, L // 32), dtype=np.uint64).astype(np.uint32)
+    P = (0.5 * rng.standard_normal((L, D))).astype(np.float32)
+    sm = 1.0 / np.sqrt(D)
+    plain = o.decode_head(q, K, V, codes, P, k, sm)
+    # no hard keys: the plain decode step
+    r = o.decode_head_eas(q, K, V, codes, P, k, np.zeros(0, np.int64), sm)
+    assert np.array_equal(r["idx"], plain["idx"]) and np.array_equal(r["union"], plain["idx"])
+    assert np.array_equal(r["out"], plain["out"])
+    # hard keys already selected by hash: nothing added, same output
+    inside = plain["idx"][::3]
+    r = o.decode_head_eas(q, K, V, codes, P, k, inside, sm)
+    assert np.all(r["added"] == 0) and np.array_equal(r["out"], plain["out"])
+    # disjoint hard keys: the union has k + m keys and attention runs over all of them
+    outside = np.setdiff1d(np.arange(N), plain["idx"])[[0, 5, 77, 200]]
+    r = o.decode_head_eas(q, K, V, codes, P, k, outside, sm)
+    assert np.all(r["added"] == 1) and r["union"].size == k + 4
+    expect = np.sort(np.concatenate([plain["idx"], outside]))
+    assert np.array_equal(r["union"], expect)
+    logits = bf16_values(q) @ bf16_values(K[expect]).T * sm
+    w = torch.softmax(torch.from_numpy(logits), dim=1).numpy()
+    assert np.allclose(r["out"], w @ bf16_values(V[expect]), rtol=1e-12, atol=1e-13)
+    # every key by hash: full attention whatever the hard set is
+    r = o.decode_head_eas(q, K, V, codes, P, N, outside, sm)
+    assert np.allclose(r["out"], o.full_attention(q, K, V, sm), rtol=1e-12, atol=1e-13)
+
+
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

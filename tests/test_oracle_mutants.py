@@ -42,6 +42,12 @@ MUTANTS = {
     "tree_sequential": ("        s = T[0:even:2] + T[1:even:2]\n", "        return np.cumsum(T, axis=0)[-1]\n"),
     "budget_floor": ("return -((-N * num) // den)", "return (N * num) // den"),
     "bf16_wrong_shift": ("<< np.uint32(16)", "<< np.uint32(15)"),
+    "hard_tie_high": ("order = np.lexsort((np.arange(N), -key))", "order = np.lexsort((-np.arange(N), -key))"),
+    "hard_smallest": ("order = np.lexsort((np.arange(N), -key))", "order = np.lexsort((np.arange(N), key))"),
+    "hard_plain_bits": ("key = np.where(u >= (1 << 31), (~u) & 0xFFFFFFFF, u | (1 << 31))", "key = u"),
+    "eas_intersection": ("union = np.union1d(idx, serr)", "union = np.intersect1d(idx, serr)"),
+    "eas_added_inverted": ("added = (~np.isin(serr, idx)).astype(np.int32)", "added = np.isin(serr, idx).astype(np.int32)"),
+    "eas_budget_floor": ("m = min(-(-budget * num // den), budget - 1)", "m = min(budget * num // den, budget - 1)"),
 }
 
 
