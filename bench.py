@@ -197,13 +197,14 @@ def main():
     for i, it in enumerate(insts):
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
         ev[0].record()
-        P, codes, _ = bpc.build_hash(it["K"], it["G"], workspace=ws_build)
+        err = torch.empty(B, Hkv, N, dtype=torch.float32, device=dev)
+        P, codes, _ = bpc.build_hash(it["K"], it["G"], err_out=err, workspace=ws_build)
         ev[1].record()
         if i == 0 and not args.no_prefill:
             codes2, _ = bpc.hash_keys(it["K"], P)
         ev[2].record()
         torch.cuda.synchronize()
-        it["P"], it["codes"] = P, codes
+        it["P"], it["codes"], it["err"] = P, codes, err
         if i == 0 and not args.no_prefill:
             build_ms = ev[0].elapsed_time(ev[1])
             hash_ms = ev[1].elapsed_time(ev[2])
@@ -265,6 +266,37 @@ def main():
     stages = {n: round(float(t) * 1e3, 2) for n, t in zip(bpc.DECODE_STAGE_NAMES, stage_ms)}  # microseconds
     log(f"stages (us): {stages}")
 
+    # ---------------------------------------------------------------- the error-aware safeguard (context)
+    # the same step with 10 % of the 2 % budget reserved for the hard-to-hash
+    # set: k_hash = 2359 by hash score, union with the 263 keys of largest
+    # reconstruction error chosen once at prefill
+    k_hash = k - (k + 9) // 10
+    m_eas = k - k_hash
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    ev[0].record()
+    for it in insts:
+        it["serr"] = bpc.select_hard(it["err"], m_eas)
+    ev[1].record()
+    torch.cuda.synchronize()
+    select_ms = ev[0].elapsed_time(ev[1]) / len(insts)
+    for j in range(args.warmup):
+        it = insts[j % len(insts)]
+        bpc.decode_attention(it["q"], it["K"], it["V"], it["codes"], it["P"], k_hash, sm, out=outs[j % len(insts)],
+                             serr=it["serr"], workspace=ws)
+    eas_steps = max(10, min(args.steps, 100))
+    ev[0].record()
+    for j in range(eas_steps):
+        it = insts[j % len(insts)]
+        bpc.decode_attention(it["q"], it["K"], it["V"], it["codes"], it["P"], k_hash, sm, out=outs[j % len(insts)],
+                             serr=it["serr"], workspace=ws)
+    ev[1].record()
+    torch.cuda.synchronize()
+    eas = {"us_per_step": round(ev[0].elapsed_time(ev[1]) / eas_steps * 1e3, 2), "k_hash": k_hash, "m": m_eas,
+           "select_hard_ms": round(select_ms, 3),
+           "what": "decode step over S_hash (top-2359 by hash score) united with S_err (263 keys of largest "
+                   "reconstruction error, chosen per (b, h) at prefill by select_hard)"}
+    log(f"safeguard: {eas}")
+
     # algorithmic bytes (per step): codes read, gathered K+V rows, P, q and out
     BH = B * Hkv
     code_bytes = BH * N * W * 4
@@ -314,6 +346,7 @@ def main():
         "stages_us": stages,
         "roofline": roofline,
         "prefill": prefill,
+        "eas": eas,
         "cpu_baseline": cpu,
         "wall_s_timed": round(wall, 4),
     }

@@ -185,6 +185,59 @@ int bpc_decode_attention(const uint16_t* q,
                          void* stream);
 
 /*
+ * bpc_select_hard -- the hard-to-hash set of the Error-Aware Safeguard
+ * (Sec. 3.2 "Error-Aware Safeguard (EAS)", Eq. reconstruction_error): for
+ * every (b, KV head), the m keys with the largest reconstruction errors
+ * ||k - h P|| (the err_out of bpc_build_hash or bpc_hash_keys).  Errors are
+ * compared in the IEEE total order of float32; equal errors go to the lower
+ * index.
+ *
+ * err       [B, Hkv, N] fp32, strides sE_b, sE_h (elements), keys contiguous
+ * m         0 <= m <= N (m = 0: nothing is written)
+ * serr_out  [B, Hkv, m] int32, contiguous: the selected key indices in
+ *           ascending order (written)
+ * Both pointers 4-byte aligned.  No workspace; one kernel launch (one
+ * workgroup per (b, KV head) making four passes over its N errors).
+ */
+int bpc_select_hard(const float* err, int64_t sE_b, int64_t sE_h, int B, int Hkv, int N, int m,
+                    int32_t* serr_out, void* stream);
+
+/*
+ * bpc_decode_attention_eas -- bpc_decode_attention with the Error-Aware
+ * Safeguard (Sec. 3.2, Eq. safeguard_union): attention runs over
+ * S_attn = S_hash u S_err, where S_hash are the k keys with the highest hash
+ * scores (selected exactly as by bpc_decode_attention) and S_err is the
+ * caller's hard-to-hash set (from bpc_select_hard at prefill).  The paper
+ * reserves 10 % of the token budget for S_err: with a budget of n keys the
+ * caller passes m = ceil(n / 10) hard keys and k = n - m.  |S_attn| is
+ * between k and k + m.
+ *
+ * serr      [B, Hkv, m] int32 with strides sS_b, sS_h: per (b, h) distinct
+ *           key indices in [0, N) in ascending order (bpc_select_hard's
+ *           output has this form; entries outside [0, N) are ignored)
+ * m         0 <= m <= N; m = 0 is bpc_decode_attention
+ * idx_out   [B, Hkv, k] int32: S_hash, ascending (or NULL)
+ * added_out [B, Hkv, m] int32 contiguous: 1 where the entry of S_err was
+ *           not in S_hash and was added, 0 where it was already selected
+ *           (or NULL)
+ * All other arguments, the workspace size and the error behaviour are those
+ * of bpc_decode_attention.
+ */
+int bpc_decode_attention_eas(const uint16_t* q,
+                             const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t sK_n,
+                             const uint16_t* V, int64_t sV_b, int64_t sV_h, int64_t sV_n,
+                             const uint32_t* codes, int64_t sC_b, int64_t sC_h,
+                             const float* P, int64_t sP_b, int64_t sP_h,
+                             int B, int Hq, int Hkv, int N, int D, int L, int k,
+                             float sm_scale,
+                             const int32_t* serr, int64_t sS_b, int64_t sS_h, int m,
+                             float* out,
+                             int32_t* idx_out,
+                             int32_t* added_out,
+                             void* workspace, size_t workspace_bytes,
+                             void* stream);
+
+/*
  * bpc_decode_attention_profiled -- bpc_decode_attention that also records
  * caller-created hipEvent_t handles on `stream` at the stage boundaries
  * (query packing | scoring | threshold, selection and attention | merge):

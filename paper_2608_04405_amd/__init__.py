@@ -24,6 +24,7 @@ __all__ = [
     "hash_keys",
     "decode_attention",
     "decode_workspace_bytes",
+    "select_hard",
     "DECODE_STAGES",
     "DECODE_STAGE_NAMES",
     "version",
@@ -57,6 +58,12 @@ _DECODE_ARGS = [_p, _p, _i64, _i64, _i64, _p, _i64, _i64, _i64, _p, _i64, _i64, 
                 _i, _i, _i, _i, _i, _i, _i, ctypes.c_float, _p, _p, _p, _p, _p, _sz, _p]
 _lib.bpc_decode_attention.restype = _i
 _lib.bpc_decode_attention.argtypes = _DECODE_ARGS
+_lib.bpc_decode_attention_eas.restype = _i
+_lib.bpc_decode_attention_eas.argtypes = [_p, _p, _i64, _i64, _i64, _p, _i64, _i64, _i64, _p, _i64, _i64, _p, _i64, _i64,
+                                          _i, _i, _i, _i, _i, _i, _i, ctypes.c_float, _p, _i64, _i64, _i, _p, _p, _p,
+                                          _p, _sz, _p]
+_lib.bpc_select_hard.restype = _i
+_lib.bpc_select_hard.argtypes = [_p, _i64, _i64, _i, _i, _i, _i, _p, _p]
 _lib.bpc_decode_attention_profiled.restype = _i
 _lib.bpc_decode_attention_profiled.argtypes = _DECODE_ARGS + [ctypes.POINTER(_p), _i]
 
@@ -190,6 +197,7 @@ def decode_attention(q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, codes: t
                      P: torch.Tensor, k: int, sm_scale: Optional[float] = None, N: Optional[int] = None, *,
                      out: Optional[torch.Tensor] = None, idx_out: Optional[torch.Tensor] = None,
                      score_out: Optional[torch.Tensor] = None, qcode_out: Optional[torch.Tensor] = None,
+                     serr: Optional[torch.Tensor] = None, added_out: Optional[torch.Tensor] = None,
                      workspace: Optional[torch.Tensor] = None, stream=None,
                      events: Optional[Sequence] = None) -> torch.Tensor:
     """One BinaryPC decode step; returns out [B, Hq, 128] fp32.
@@ -199,7 +207,12 @@ def decode_attention(q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, codes: t
     [L, 128]).  Optional debug outputs: idx_out [B, Hkv, k] int32,
     score_out [B, Hkv, N] int32, qcode_out [B, Hkv, 8, L/32] int32.
     `events`: BPC_DECODE_STAGES + 1 torch.cuda.Event objects recorded at the
-    stage boundaries (for measurement)."""
+    stage boundaries (for measurement).
+
+    With `serr` [B, Hkv, m] int32 (the hard-to-hash set from select_hard),
+    attention runs over the union of the k hash-selected keys and serr (the
+    error-aware safeguard); added_out [B, Hkv, m] int32 then marks the
+    entries of serr that the hash selection had not taken."""
     _need(q, "q", torch.bfloat16, 3)
     _need(K, "K", torch.bfloat16, 4)
     _need(V, "V", torch.bfloat16, 4)
@@ -226,7 +239,20 @@ def decode_attention(q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, codes: t
             codes.stride(1), _ptr(P), sPb, sPh, B, Hq, Hkv, N, D, L, k, float(sm_scale), _ptr(out),
             _ptr(idx_out), _ptr(score_out), _ptr(qcode_out), _ptr(workspace), workspace.numel(),
             _stream(stream)]
-    if events is None:
+    if serr is not None:
+        if events is not None or score_out is not None or qcode_out is not None:
+            raise ValueError("serr cannot be combined with events, score_out or qcode_out")
+        if serr.dtype != torch.int32 or serr.dim() != 3 or serr.stride(-1) != 1 or serr.device != q.device:
+            raise ValueError("serr must be a [B, Hkv, m] int32 tensor on the GPU, innermost dimension contiguous")
+        m = serr.shape[-1]
+        if added_out is not None and (added_out.dtype != torch.int32 or not added_out.is_contiguous()
+                                      or tuple(added_out.shape) != (B, Hkv, m)):
+            raise ValueError("added_out must be a contiguous [B, Hkv, m] int32 tensor")
+        _check(_lib.bpc_decode_attention_eas(*args[:23], _ptr(serr), serr.stride(0), serr.stride(1), m, _ptr(out),
+                                             _ptr(idx_out), _ptr(added_out), _ptr(workspace), workspace.numel(),
+                                             _stream(stream)),
+               "bpc_decode_attention_eas")
+    elif events is None:
         _check(_lib.bpc_decode_attention(*args), "bpc_decode_attention")
     else:
         handles = (_p * len(events))()
@@ -237,3 +263,21 @@ def decode_attention(q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, codes: t
             handles[i] = ev.cuda_event
         _check(_lib.bpc_decode_attention_profiled(*args, handles, len(events)), "bpc_decode_attention_profiled")
     return out
+
+
+def select_hard(err: torch.Tensor, m: int, N: Optional[int] = None, *, serr_out: Optional[torch.Tensor] = None,
+                stream=None) -> torch.Tensor:
+    """The error-aware safeguard's hard-to-hash set: per (b, KV head), the m
+    keys with the largest reconstruction errors (err [B, Hkv, >=N] fp32, as
+    written by build_hash / hash_keys), ascending; returns [B, Hkv, m] int32."""
+    _need(err, "err", torch.float32, 3)
+    B, Hkv, Ncap = err.shape
+    N = Ncap if N is None else N
+    if serr_out is None:
+        serr_out = torch.empty(B, Hkv, max(m, 0), dtype=torch.int32, device=err.device)
+    elif serr_out.dtype != torch.int32 or not serr_out.is_contiguous() or tuple(serr_out.shape) != (B, Hkv, m):
+        raise ValueError("serr_out must be a contiguous [B, Hkv, m] int32 tensor")
+    _check(_lib.bpc_select_hard(_ptr(err), err.stride(0), err.stride(1), B, Hkv, N, m, _ptr(serr_out),
+                                _stream(stream)),
+           "bpc_select_hard")
+    return serr_out

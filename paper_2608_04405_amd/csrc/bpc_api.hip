@@ -28,6 +28,7 @@ static int hip_fail(hipError_t e, const char* what) {
 static size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 static bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+static bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
 
 static int check_code_len(int L) {
   if (L != 32 && L != 64 && L != 128) return fail(BPC_EUNSUPPORTED, "L=%d: code length must be 32, 64 or 128", L);
@@ -90,7 +91,6 @@ DecodeLayout decode_layout(int B, int Hq, int Hkv, int N, int L, int k) {
   d.off_hist_cc = take(S * (size_t)kCoarseStride * sizeof(uint32_t));
   d.off_win = take(S * (size_t)kWinRec * sizeof(uint32_t));
   d.off_part = take(S * d.G * (kHeadDim + 2) * sizeof(float));
-  d.off_idx = take(BH * (size_t)k * sizeof(int32_t));
   d.off_qcode = take(BH * kQcodeStride * sizeof(uint32_t));
   d.total = o;
   return d;
@@ -196,8 +196,9 @@ static int decode_impl(const uint16_t* q, const uint16_t* K, int64_t sK_b, int64
                        const uint16_t* V, int64_t sV_b, int64_t sV_h, int64_t sV_n, const uint32_t* codes,
                        int64_t sC_b, int64_t sC_h, const float* P, int64_t sP_b, int64_t sP_h, int B, int Hq,
                        int Hkv, int N, int D, int L, int k, float sm_scale, float* out, int32_t* idx_out,
-                       int32_t* score_out, uint32_t* qcode_out, void* workspace, size_t workspace_bytes,
-                       void* stream, void* const* events, int n_events) {
+                       int32_t* score_out, uint32_t* qcode_out, const int32_t* serr, int64_t sS_b, int64_t sS_h,
+                       int m, int32_t* added_out, void* workspace, size_t workspace_bytes, void* stream,
+                       void* const* events, int n_events) {
   g_last_error[0] = 0;
   int st;
   if ((st = check_sizes(B, Hkv, N))) return st;
@@ -227,6 +228,12 @@ static int decode_impl(const uint16_t* q, const uint16_t* K, int64_t sK_b, int64
   if ((st = check_opt_aligned("idx_out", idx_out))) return st;
   if ((st = check_opt_aligned("score_out", score_out))) return st;
   if ((st = check_opt_aligned("qcode_out", qcode_out))) return st;
+  if (m < 0 || m > N) return fail(BPC_EINVAL, "m=%d must satisfy 0 <= m <= N=%d", m, N);
+  if (m > 0) {
+    if (!serr) return fail(BPC_EINVAL, "serr is required when m > 0");
+    if (sS_b < 0 || sS_h < 0) return fail(BPC_EINVAL, "serr strides must be >= 0");
+    if ((st = check_opt_aligned("added_out", added_out))) return st;
+  }
   if (events && n_events != BPC_DECODE_STAGES + 1)
     return fail(BPC_EINVAL, "n_events=%d, expected %d", n_events, BPC_DECODE_STAGES + 1);
   const DecodeLayout lay = decode_layout(B, Hq, Hkv, N, L, k);
@@ -244,6 +251,7 @@ static int decode_impl(const uint16_t* q, const uint16_t* K, int64_t sK_b, int64
   a.B = B, a.Hq = Hq, a.Hkv = Hkv, a.N = N, a.L = L, a.k = k;
   a.sm_scale = sm_scale;
   a.out = out, a.idx_out = idx_out, a.score_out = score_out, a.qcode_out = qcode_out;
+  a.serr = m > 0 ? serr : nullptr, a.sS_b = sS_b, a.sS_h = sS_h, a.m = m, a.added_out = m > 0 ? added_out : nullptr;
   a.ws = static_cast<char*>(workspace);
   a.stream = static_cast<hipStream_t>(stream);
   a.events = reinterpret_cast<hipEvent_t const*>(events);
@@ -259,8 +267,34 @@ int bpc_decode_attention(const uint16_t* q, const uint16_t* K, int64_t sK_b, int
                          int32_t* score_out, uint32_t* qcode_out, void* workspace, size_t workspace_bytes,
                          void* stream) {
   return decode_impl(q, K, sK_b, sK_h, sK_n, V, sV_b, sV_h, sV_n, codes, sC_b, sC_h, P, sP_b, sP_h, B, Hq, Hkv,
-                     N, D, L, k, sm_scale, out, idx_out, score_out, qcode_out, workspace, workspace_bytes, stream,
-                     nullptr, 0);
+                     N, D, L, k, sm_scale, out, idx_out, score_out, qcode_out, nullptr, 0, 0, 0, nullptr, workspace,
+                     workspace_bytes, stream, nullptr, 0);
+}
+
+int bpc_decode_attention_eas(const uint16_t* q, const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t sK_n,
+                             const uint16_t* V, int64_t sV_b, int64_t sV_h, int64_t sV_n, const uint32_t* codes,
+                             int64_t sC_b, int64_t sC_h, const float* P, int64_t sP_b, int64_t sP_h, int B, int Hq,
+                             int Hkv, int N, int D, int L, int k, float sm_scale, const int32_t* serr, int64_t sS_b,
+                             int64_t sS_h, int m, float* out, int32_t* idx_out, int32_t* added_out,
+                             void* workspace, size_t workspace_bytes, void* stream) {
+  return decode_impl(q, K, sK_b, sK_h, sK_n, V, sV_b, sV_h, sV_n, codes, sC_b, sC_h, P, sP_b, sP_h, B, Hq, Hkv,
+                     N, D, L, k, sm_scale, out, idx_out, nullptr, nullptr, serr, sS_b, sS_h, m, added_out, workspace,
+                     workspace_bytes, stream, nullptr, 0);
+}
+
+int bpc_select_hard(const float* err, int64_t sE_b, int64_t sE_h, int B, int Hkv, int N, int m, int32_t* serr_out,
+                    void* stream) {
+  g_last_error[0] = 0;
+  int st;
+  if ((st = check_sizes(B, Hkv, N))) return st;
+  if (m < 0 || m > N) return fail(BPC_EINVAL, "m=%d must satisfy 0 <= m <= N=%d", m, N);
+  if (m == 0) return BPC_OK;
+  if (!err || !serr_out) return fail(BPC_EINVAL, "err and serr_out are required");
+  if (sE_b < 0 || sE_h < 0) return fail(BPC_EINVAL, "err strides must be >= 0");
+  if (!aligned4(err) || !aligned4(serr_out)) return fail(BPC_EALIGN, "err and serr_out must be 4-byte aligned");
+  hipError_t e = launch_select_hard(err, sE_b, sE_h, B, Hkv, N, m, serr_out, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "bpc_select_hard launch");
+  return BPC_OK;
 }
 
 int bpc_decode_attention_profiled(const uint16_t* q, const uint16_t* K, int64_t sK_b, int64_t sK_h,
@@ -274,8 +308,8 @@ int bpc_decode_attention_profiled(const uint16_t* q, const uint16_t* K, int64_t 
   for (int i = 0; i < n_events; ++i)
     if (!events[i]) return fail(BPC_EINVAL, "events[%d] is NULL", i);
   return decode_impl(q, K, sK_b, sK_h, sK_n, V, sV_b, sV_h, sV_n, codes, sC_b, sC_h, P, sP_b, sP_h, B, Hq, Hkv,
-                     N, D, L, k, sm_scale, out, idx_out, score_out, qcode_out, workspace, workspace_bytes, stream,
-                     events, n_events);
+                     N, D, L, k, sm_scale, out, idx_out, score_out, qcode_out, nullptr, 0, 0, 0, nullptr, workspace,
+                     workspace_bytes, stream, events, n_events);
 }
 
 }  // extern "C"

@@ -58,12 +58,13 @@ constexpr int kBuildRows = 256;  // rows per workgroup in the build passes
 // [fine_stride] u32, coarse
 // prefix [kCoarseStride] u32, window record [kWinRec] u32 and G partials of
 // (max, sum, o[128]) fp32; per (b, h) the packed query (8 W plane words,
-// then sum |p|; stride kQcodeStride) and the k selected indices (used when
-// the caller passes no idx_out and a slice keeps more rows than LDS holds).
+// then sum |p|; stride kQcodeStride).  When a slice keeps more rows than its
+// LDS list holds, the attention kernel writes them over the slice's own
+// candidate area (a kept entry's rank never exceeds its position there).
 constexpr int kQcodeStride = 64;
 struct DecodeLayout {
   int nslices, G, W;
-  size_t off_cand, off_meta, off_hist_fine, off_hist_cc, off_win, off_part, off_idx, off_qcode, total;
+  size_t off_cand, off_meta, off_hist_fine, off_hist_cc, off_win, off_part, off_qcode, total;
 };
 
 struct BuildLayout {
@@ -91,12 +92,19 @@ struct DecodeArgs {
   int32_t* idx_out;
   int32_t* score_out;
   uint32_t* qcode_out;
+  const int32_t* serr;  // error-aware safeguard: [B, Hkv, m] ascending, or nullptr
+  int64_t sS_b, sS_h;
+  int m;
+  int32_t* added_out;
   char* ws;
   hipStream_t stream;
   hipEvent_t const* events;  // BPC_DECODE_STAGES + 1 handles, or nullptr
 };
 
 hipError_t launch_decode(const DecodeArgs& a);
+
+hipError_t launch_select_hard(const float* err, int64_t sE_b, int64_t sE_h, int B, int Hkv, int N, int m,
+                              int32_t* out, hipStream_t stream);
 
 hipError_t launch_hash(const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t sK_n, int B, int Hkv,
                        int N, int L, const float* P, int64_t sP_b, int64_t sP_h, uint32_t* codes,
@@ -120,5 +128,39 @@ __device__ __forceinline__ double dadd(double a, double b) { return a + b; }
 __device__ __forceinline__ double dmul(double a, double b) { return a * b; }
 
 __device__ __forceinline__ bool fragile_decision(double a) { return fabsf((float)a) < 1e-6f; }
+
+// ---------------------------------------------------------------------------
+// block-wide exclusive scan of one int per thread (NT threads, wave64)
+// ---------------------------------------------------------------------------
+template <int NT>
+__device__ __forceinline__ int block_exclusive_scan(int v, int* wave_tot, int& total) {
+  constexpr int NW = NT / 64;
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  int x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) wave_tot[wid] = x;
+  __syncthreads();
+  if (wid == 0) {
+    int t = (lane < NW) ? wave_tot[lane] : 0;
+#pragma unroll
+    for (int o = 1; o < NW; o <<= 1) {
+      const int y = __shfl_up(t, o, 64);
+      if (lane >= o) t += y;
+    }
+    if (lane < NW) wave_tot[lane] = t;  // inclusive prefix of wave totals
+  }
+  __syncthreads();
+  const int before = (wid > 0) ? wave_tot[wid - 1] : 0;
+  total = wave_tot[NW - 1];
+  __syncthreads();  // wave_tot may be reused right after
+  return before + x - v;
+}
+
+// lowest set lane of a 64-bit ballot, or 64
+__device__ __forceinline__ int first_lane(unsigned long long m) { return m ? __ffsll((long long)m) - 1 : 64; }
 
 }  // namespace bpc

@@ -56,40 +56,6 @@ __device__ unsigned long long* g_trace = nullptr;
 #define BPC_NOTE(kern, slot, val) ((void)0)
 #endif
 
-// ---------------------------------------------------------------------------
-// block-wide exclusive scan of one int per thread (NT threads, wave64)
-// ---------------------------------------------------------------------------
-template <int NT>
-__device__ __forceinline__ int block_exclusive_scan(int v, int* wave_tot, int& total) {
-  constexpr int NW = NT / 64;
-  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-  int x = v;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int y = __shfl_up(x, o, 64);
-    if (lane >= o) x += y;
-  }
-  if (lane == 63) wave_tot[wid] = x;
-  __syncthreads();
-  if (wid == 0) {
-    int t = (lane < NW) ? wave_tot[lane] : 0;
-#pragma unroll
-    for (int o = 1; o < NW; o <<= 1) {
-      const int y = __shfl_up(t, o, 64);
-      if (lane >= o) t += y;
-    }
-    if (lane < NW) wave_tot[lane] = t;  // inclusive prefix of wave totals
-  }
-  __syncthreads();
-  const int before = (wid > 0) ? wave_tot[wid - 1] : 0;
-  total = wave_tot[NW - 1];
-  __syncthreads();  // wave_tot may be reused right after
-  return before + x - v;
-}
-
-// lowest set lane of a 64-bit ballot, or 64
-__device__ __forceinline__ int first_lane(unsigned long long m) { return m ? __ffsll((long long)m) - 1 : 64; }
-
 // Workgroup id -> (b, h) and slice.  Workgroups are dispatched to the eight
 // XCDs round-robin by id; all slices of one (b, h) get ids with the same
 // residue mod 8, so they run on one XCD and share its L2 (P, q, candidates).
@@ -707,7 +673,8 @@ struct AttendShared {
   int wave_tot[kAttnWaves];
   int first[2];
   int red[2][kAttnWaves];
-  int plan3[3];  // one-round threshold: take, off, kept of this slice
+  int plan3[3];               // one-round threshold: take, off, kept of this slice
+  uint32_t sel[kSlice / 32];  // the safeguard: bitmap of the slice's keys the hash selection took
 };
 
 // One pass of a wavefront over nrows (1..kAttnRows) rows; lane l < nrows
@@ -795,7 +762,8 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(G 
     int N, int k, int L, int BH, int Hkv, int nslices, int win_ok, const uint32_t* __restrict__ cand,
     const uint32_t* __restrict__ meta, const uint32_t* __restrict__ hist_fine, const uint32_t* __restrict__ hist_cc,
     const uint32_t* __restrict__ win, const uint32_t* __restrict__ codes, int64_t sC_b, int64_t sC_h,
-    const uint32_t* __restrict__ qcode, int32_t* __restrict__ idx, int write_idx, const uint16_t* __restrict__ q,
+    const uint32_t* __restrict__ qcode, int32_t* __restrict__ idx_out, const int32_t* __restrict__ serr, int64_t sS_b,
+    int64_t sS_h, int m, int32_t* __restrict__ added_out, const uint16_t* __restrict__ q,
     const uint16_t* __restrict__ K, int64_t sK_b, int64_t sK_h, int64_t sK_n, const uint16_t* __restrict__ V,
     int64_t sV_b, int64_t sV_h, int64_t sV_n, float scale_log2, float* __restrict__ part) {
   constexpr int PER = kCandBatch / kAttnThreads;  // candidates per thread per batch
@@ -1047,16 +1015,20 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(G 
   kept = min(kept, k - off);
   BPC_STAMP(2, 3);
 
-  // ---- b. selection: the kept candidates, in ascending key order, go to
-  // the slice's range [off, off + kept) of the index list: to the LDS row
-  // list when it holds them, and to global memory when it does not or when
-  // the caller asked for the indices
-  // In the one-round path the entries are the slice's candidate list (it
-  // holds every key with distance <= T* since T* <= hi <= cand_max_s);
-  // otherwise the slice's codes are scored again.
-  const bool rows_lds = kept <= kRowCache;
-  const bool rows_glb = !rows_lds || write_idx;
-  int32_t* grows = idx + (size_t)bh * k + off;
+  // ---- b. selection: the kept entries, in ascending key order, go to the
+  // slice's row list (in LDS when it holds them and the safeguard keys,
+  // else over the slice's own candidate area: a kept entry's rank never
+  // exceeds its position there, and the safeguard keys are appended after
+  // every candidate has been read) and, when the caller asks for them, to
+  // [off, off + kept) of the (b, h) index list.  In the one-round path the
+  // entries are the slice's candidate list (it holds every key with distance
+  // <= T* since T* <= hi <= cand_max_s); otherwise the slice's codes are
+  // scored again.
+  const bool rows_lds = kept + m <= kRowCache;
+  int32_t* grows = reinterpret_cast<int32_t*>(const_cast<uint32_t*>(cs));
+  int32_t* xrows = idx_out ? idx_out + (size_t)bh * k + off : nullptr;
+  if (m > 0)
+    for (int i = threadIdx.x; i < kSlice / 32; i += kAttnThreads) sh.sel[i] = 0u;  // ordered by the scan's barriers
   const int nent = planned ? ncand : min(kSlice, N - n0);
   const int W = L / 32;
   uint32_t sg[4] = {0u, 0u, 0u, 0u}, M[7][4] = {};
@@ -1117,9 +1089,13 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(G 
         ++tie_rank;
       }
       if (keep && rank < kept) {
-        const int key = n0 + (int)(cv[e] >> 16);
-        if (rows_lds) sh.u.rows[rank] = key;
-        if (rows_glb) grows[rank] = key;
+        const int kin = (int)(cv[e] >> 16);
+        if (rows_lds)
+          sh.u.rows[rank] = n0 + kin;
+        else
+          grows[rank] = n0 + kin;
+        if (xrows) xrows[rank] = n0 + kin;
+        if (m > 0) atomicOr(&sh.sel[kin >> 5], 1u << (kin & 31));
       }
       rank += keep;
     }
@@ -1127,6 +1103,42 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(G 
     tie_seen += tot >> 16;
   }
   __syncthreads();  // the list is complete and visible to the whole workgroup
+
+  // ---- error-aware safeguard: the keys of S_err in this slice that the hash
+  // selection did not take are appended to the row list (in S_err order,
+  // which is ascending); added_out marks them
+  if (m > 0) {
+    const int32_t* se = serr + b * sS_b + h * sS_h;
+    const int cnt = min(kSlice, N - n0);
+    int extra = 0;
+    for (int base = 0; base < m; base += 4 * kAttnThreads) {
+      int key[4], add[4], na = 0;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int j = base + 4 * (int)threadIdx.x + u;
+        key[u] = (j < m) ? se[j] : -1;
+        const int kin = key[u] - n0;
+        const bool here = key[u] >= n0 && kin < cnt;
+        add[u] = here && !((sh.sel[kin >> 5] >> (kin & 31)) & 1u);
+        if (here && added_out) added_out[(size_t)bh * m + j] = add[u];
+        na += add[u];
+      }
+      int tot;
+      int pos = kept + extra + block_exclusive_scan<kAttnThreads>(na, sh.wave_tot, tot);
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (add[u]) {
+          if (rows_lds)
+            sh.u.rows[pos] = key[u];  // pos < kept + m <= kRowCache
+          else if (pos < kSlice)      // (repeated S_err entries could overrun the area)
+            grows[pos] = key[u];
+          ++pos;
+        }
+      extra += tot;
+    }
+    kept = min(kept + extra, rows_lds ? kRowCache : kSlice);
+    __syncthreads();
+  }
   BPC_STAMP(2, 4);
 
   // ---- c. attention: wavefront wid takes rows [16 (wid + 4 i), 16 (wid + 4 i) + 16)
@@ -1261,7 +1273,6 @@ static hipError_t launch_decode_L(const DecodeArgs& a, const DecodeLayout& lay) 
   uint32_t* hist_cc = reinterpret_cast<uint32_t*>(a.ws + lay.off_hist_cc);
   uint32_t* win = reinterpret_cast<uint32_t*>(a.ws + lay.off_win);
   float* part = reinterpret_cast<float*>(a.ws + lay.off_part);
-  int32_t* idx = a.idx_out ? a.idx_out : reinterpret_cast<int32_t*>(a.ws + lay.off_idx);
   uint32_t* qcode = reinterpret_cast<uint32_t*>(a.ws + lay.off_qcode);
   const float scale_log2 = a.sm_scale * 1.4426950408889634f;
   hipStream_t st = a.stream;
@@ -1287,8 +1298,8 @@ static hipError_t launch_decode_L(const DecodeArgs& a, const DecodeLayout& lay) 
 #define BPC_ATTEND_CASE(GG)                                                                                     \
   case GG:                                                                                                      \
     attend_kernel<GG><<<nwg, kAttnThreads, 0, st>>>(a.N, a.k, L, BH, a.Hkv, lay.nslices, win_ok, cand, meta,    \
-                                                    hist_fine, hist_cc, win, a.codes, a.sC_b, a.sC_h, qcode, idx, \
-                                                    a.idx_out != nullptr, a.q, a.K,                               \
+                                                    hist_fine, hist_cc, win, a.codes, a.sC_b, a.sC_h, qcode,      \
+                                                    a.idx_out, a.serr, a.sS_b, a.sS_h, a.m, a.added_out, a.q, a.K, \
                                                     a.sK_b, a.sK_h, a.sK_n, a.V, a.sV_b, a.sV_h, a.sV_n,          \
                                                     scale_log2, part);                                            \
     break;

@@ -159,3 +159,64 @@ def _build(lib, **kw):
 ])
 def test_build_rejects(lib, kw, code):
     assert _build(lib, **kw) == code
+
+
+def _select_hard(lib, **kw):
+    a = dict(err=FAKE, sEb=8 * 4096, sEh=4096, B=1, Hkv=8, N=4096, m=9, out=FAKE, stream=None)
+    a.update(kw)
+    f = lib.bpc_select_hard
+    f.restype = ctypes.c_int
+    return f(ctypes.c_void_p(a["err"]), _i64(a["sEb"]), _i64(a["sEh"]), a["B"], a["Hkv"], a["N"], a["m"],
+             ctypes.c_void_p(a["out"]), ctypes.c_void_p(a["stream"]))
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(err=None), EINVAL),
+    (dict(out=None), EINVAL),
+    (dict(B=0), EINVAL),
+    (dict(m=-1), EINVAL),
+    (dict(m=4097), EINVAL),
+    (dict(sEh=-1), EINVAL),
+    (dict(err=FAKE + 2), EALIGN),
+    (dict(out=FAKE + 1), EALIGN),
+])
+def test_select_hard_rejects(lib, kw, code):
+    assert _select_hard(lib, **kw) == code
+    assert lib.bpc_last_error() != b""
+
+
+def test_select_hard_empty_set_launches_nothing(lib):
+    # m = 0 selects nothing: success without touching the (fake) pointers
+    assert _select_hard(lib, m=0, err=None, out=None) == OK
+
+
+def _decode_eas(lib, **kw):
+    a = dict(q=FAKE, K=FAKE, sKb=8 * 4096 * 128, sKh=4096 * 128, sKn=128, V=FAKE, sVb=8 * 4096 * 128,
+             sVh=4096 * 128, sVn=128, codes=FAKE, sCb=8 * 4096, sCh=4096, P=FAKE, sPb=8 * 32 * 128, sPh=32 * 128,
+             B=1, Hq=8, Hkv=8, N=4096, D=128, L=32, k=74, sm=0.088, serr=FAKE, sSb=8 * 8, sSh=8, m=8, out=FAKE,
+             idx=None, added=None, ws=FAKE, ws_bytes=0, stream=None)
+    a.update(kw)
+    f = lib.bpc_decode_attention_eas
+    f.restype = ctypes.c_int
+    return f(ctypes.c_void_p(a["q"]), ctypes.c_void_p(a["K"]), _i64(a["sKb"]), _i64(a["sKh"]), _i64(a["sKn"]),
+             ctypes.c_void_p(a["V"]), _i64(a["sVb"]), _i64(a["sVh"]), _i64(a["sVn"]), ctypes.c_void_p(a["codes"]),
+             _i64(a["sCb"]), _i64(a["sCh"]), ctypes.c_void_p(a["P"]), _i64(a["sPb"]), _i64(a["sPh"]), a["B"],
+             a["Hq"], a["Hkv"], a["N"], a["D"], a["L"], a["k"], ctypes.c_float(a["sm"]), ctypes.c_void_p(a["serr"]),
+             _i64(a["sSb"]), _i64(a["sSh"]), a["m"], ctypes.c_void_p(a["out"]), ctypes.c_void_p(a["idx"]),
+             ctypes.c_void_p(a["added"]), ctypes.c_void_p(a["ws"]), ctypes.c_size_t(a["ws_bytes"]),
+             ctypes.c_void_p(a["stream"]))
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(serr=None), EINVAL),       # m > 0 needs the hard set
+    (dict(m=-1), EINVAL),
+    (dict(m=4097), EINVAL),
+    (dict(sSh=-8), EINVAL),
+    (dict(added=FAKE + 4), EALIGN),
+    (dict(k=0), EINVAL),
+    (dict(q=None), EINVAL),
+    (dict(ws_bytes=1024), EWS),
+])
+def test_decode_eas_rejects(lib, kw, code):
+    assert _decode_eas(lib, **kw) == code
+    assert lib.bpc_last_error() != b""

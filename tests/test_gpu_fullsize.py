@@ -7,6 +7,8 @@ outputs that the oracle can afford, and through properties on every head.
   GPU build + decode of the whole batch; one sampled (sequence, KV head) is
   rebuilt by the oracle (projection and codes bit-exact) and decoded by the
   oracle (query planes, scores, indices bit-exact; output within 2e-3).
+  The same head is then decoded with the error-aware safeguard (10 % of
+  the budget for the hard-to-hash set) against the oracle.
 * stack32_b8_64k, one layer (batch 8, 65536 keys, top-1311): the same for the
   build, plus Algorithm 2 on sampled keys (each key hashes independently).
 * million_1m (1 048 576 keys, 128-bit codes, top-10486): the oracle cannot
@@ -110,7 +112,7 @@ def compare_sampled_head(d, P_ref, codes_ref, b, h, cfg, out, idx, sc, qc, label
     assert np.all(e <= TOL), f"{label}: output error {e.max():.3g}"
 
 
-def build_decode_case(name, sample, hash_rows):
+def build_decode_case(name, sample, hash_rows, eas=False):
     cfg = config_by_name(name)
     announce(f"[full size] {cfg}")
     d = make_layer(cfg, device=DEV)
@@ -127,6 +129,28 @@ def build_decode_case(name, sample, hash_rows):
     assert np.array_equal(u32(codes[b, h]), codes_ref), f"{name}: codes differ at {(b, h)}"
     np.testing.assert_allclose(err[b, h].cpu().numpy(), err_ref, rtol=1e-5, atol=1e-4)
     compare_sampled_head(d, P_ref, codes_ref, b, h, cfg, out, idx, sc, qc, f"{name} head {(b, h)}")
+    if eas:
+        # the safeguard at full size: 10 % of the budget for the hard set,
+        # chosen on the GPU from the GPU build's errors (the same float32
+        # errors go to the oracle's selection)
+        k_hash, m = oracle.eas_budget(cfg.k)
+        serr = bpc.select_hard(err, m)
+        idx2 = torch.empty(cfg.B, cfg.Hkv, k_hash, dtype=torch.int32, device=DEV)
+        added = torch.empty(cfg.B, cfg.Hkv, m, dtype=torch.int32, device=DEV)
+        out2 = bpc.decode_attention(d["q"], d["K"], d["V"], codes, P, k_hash, N=cfg.N, idx_out=idx2, serr=serr,
+                                    added_out=added)
+        torch.cuda.synchronize()
+        serr_n = serr[b, h].cpu().numpy()
+        assert np.array_equal(serr_n, oracle.select_hard(err[b, h].cpu().numpy(), m)), f"{name}: hard set differs"
+        sm = 1.0 / np.sqrt(cfg.D)
+        ref = oracle.decode_head_eas(bits(d["q"][b, h * cfg.G:(h + 1) * cfg.G]), Kb, bits(d["V"][b, h, :cfg.N]),
+                                     codes_ref, P_ref, k_hash, serr_n, sm)
+        assert np.array_equal(idx2[b, h].cpu().numpy(), ref["idx"]), f"{name}: safeguard S_hash differs"
+        assert np.array_equal(added[b, h].cpu().numpy(), ref["added"]), f"{name}: safeguard flags differ"
+        e = rel_err(out2[b, h * cfg.G:(h + 1) * cfg.G].cpu().numpy(), ref["out"])
+        announce(f"{name} head {(b, h)} with the safeguard ({int(ref['added'].sum())} of {m} added): "
+                 f"max relative output error {e.max():.3g}")
+        assert np.all(e <= TOL)
     if hash_rows:
         rng = np.random.default_rng(cfg.seed)
         rows = np.unique(np.concatenate([rng.choice(cfg.N, hash_rows, replace=False), [0, cfg.N - 1]]))
@@ -139,7 +163,7 @@ def build_decode_case(name, sample, hash_rows):
 
 @pytest.mark.timeout(600)
 def test_fullsize_batch16_128k():
-    build_decode_case("batch16_128k", sample=(11, 6), hash_rows=0)
+    build_decode_case("batch16_128k", sample=(11, 6), hash_rows=0, eas=True)
 
 
 @pytest.mark.timeout(600)
