@@ -136,6 +136,37 @@ int bpc_hash_keys(const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t sK_n,
                   void* stream);
 
 /*
+ * bpc_append_kv -- decode-time append of T new tokens to the cache: their
+ * key and value rows are stored at positions [pos, pos + T) of K and V, and
+ * each new key is hashed against the given projection with the iterative
+ * residual of Algorithm "Given projection, computing hashcode" (Sec. 3.2:
+ * the setting "where the projection matrix P is given"), its code stored at
+ * the same positions of `codes`.  The arithmetic and the code bits are those
+ * of bpc_hash_keys.  P stays fixed, as the paper's decode phase keeps it.
+ *
+ * k_new, v_new [B, Hkv, T, D] bf16, strides (sKn_b, sKn_h, sKn_t) and
+ *            (sVn_b, sVn_h, sVn_t)
+ * K, V       [B, Hkv, Ncap, D] bf16 caches, strides as in bpc_decode_attention
+ *            (rows pos .. pos + T - 1 written)
+ * codes      [B, Hkv, Ncap, W] uint32, strides sC_b, sC_h (rows written)
+ * P          [B, Hkv, L, D] fp32, strides sP_b, sP_h (0, 0 = shared)
+ * Ncap       rows the caches hold; 0 <= pos and pos + T <= Ncap
+ * err_out    [B, Hkv, T] fp32 contiguous ||k - h P|| of the new keys (or NULL)
+ * fragile_out  device uint64 accumulator (or NULL), as for bpc_hash_keys.
+ * No workspace; one kernel launch.
+ */
+int bpc_append_kv(const uint16_t* k_new, int64_t sKn_b, int64_t sKn_h, int64_t sKn_t,
+                  const uint16_t* v_new, int64_t sVn_b, int64_t sVn_h, int64_t sVn_t,
+                  uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t sK_n,
+                  uint16_t* V, int64_t sV_b, int64_t sV_h, int64_t sV_n,
+                  uint32_t* codes, int64_t sC_b, int64_t sC_h,
+                  const float* P, int64_t sP_b, int64_t sP_h,
+                  int B, int Hkv, int Ncap, int pos, int T, int D, int L,
+                  float* err_out,
+                  unsigned long long* fragile_out,
+                  void* stream);
+
+/*
  * bpc_decode_attention -- one decode step of BinaryPC sparse attention
  * (Sec. 3.2 "Retrieval Phase"; Algorithm "Computing hashing score";
  * Sec. 4.2 "Kernel Evaluation": search, selection, gathering, attention).

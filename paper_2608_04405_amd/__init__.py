@@ -18,6 +18,7 @@ import torch
 
 __all__ = [
     "BPCError",
+    "append_kv",
     "LIB_PATH",
     "build_hash",
     "build_workspace_bytes",
@@ -62,6 +63,9 @@ _lib.bpc_decode_attention_eas.restype = _i
 _lib.bpc_decode_attention_eas.argtypes = [_p, _p, _i64, _i64, _i64, _p, _i64, _i64, _i64, _p, _i64, _i64, _p, _i64, _i64,
                                           _i, _i, _i, _i, _i, _i, _i, ctypes.c_float, _p, _i64, _i64, _i, _p, _p, _p,
                                           _p, _sz, _p]
+_lib.bpc_append_kv.restype = _i
+_lib.bpc_append_kv.argtypes = [_p, _i64, _i64, _i64, _p, _i64, _i64, _i64, _p, _i64, _i64, _i64, _p, _i64, _i64, _i64,
+                               _p, _i64, _i64, _p, _i64, _i64, _i, _i, _i, _i, _i, _i, _i, _p, _p, _p]
 _lib.bpc_select_hard.restype = _i
 _lib.bpc_select_hard.argtypes = [_p, _i64, _i64, _i, _i, _i, _i, _p, _p]
 _lib.bpc_decode_attention_profiled.restype = _i
@@ -115,6 +119,23 @@ def _kv_strides(t: torch.Tensor):
     return t.stride(0), t.stride(1), t.stride(2)
 
 
+def _proj(P: torch.Tensor, D: int = 128):
+    """(L, sP_b, sP_h) of a projection given as [B, Hkv, L, D] (one per
+    (sequence, KV head)), [Hkv, L, D] (one per KV head, shared by the batch:
+    offline calibration) or [L, D] (one for everything)."""
+    if P.dtype != torch.float32 or P.device.type != "cuda":
+        raise TypeError("P must be a float32 GPU tensor")
+    if P.stride(-1) != 1 or P.shape[-1] != D or (P.dim() >= 2 and P.shape[-2] > 1 and P.stride(-2) != D):
+        raise ValueError("P rows must be contiguous [.., L, 128]")
+    if P.dim() == 2:
+        return P.shape[0], 0, 0
+    if P.dim() == 3:
+        return P.shape[1], 0, P.stride(0)
+    if P.dim() == 4:
+        return P.shape[2], P.stride(0), P.stride(1)
+    raise ValueError("P must be [B, Hkv, L, 128], [Hkv, L, 128] or [L, 128]")
+
+
 def build_workspace_bytes(B: int, Hkv: int, N: int, L: int, D: int = 128) -> int:
     return int(_lib.bpc_build_workspace_bytes(B, Hkv, N, D, L))
 
@@ -166,23 +187,13 @@ def build_hash(K: torch.Tensor, G: torch.Tensor, N: Optional[int] = None, *,
 def hash_keys(K: torch.Tensor, P: torch.Tensor, N: Optional[int] = None, *,
               codes_out: Optional[torch.Tensor] = None, err_out: Optional[torch.Tensor] = None,
               fragile: Optional[torch.Tensor] = None, stream=None):
-    """Hash keys against P (Algorithm 2).  P is [B, Hkv, L, 128] or a shared
-    [L, 128] (broadcast with zero strides).  Returns (codes, err)."""
+    """Hash keys against P (Algorithm 2).  P is [B, Hkv, L, 128], or
+    [Hkv, L, 128] / [L, 128] shared across the batch (offline calibration).
+    Returns (codes, err)."""
     _need(K, "K", torch.bfloat16, 4)
     B, Hkv, Ncap, D = K.shape
     N = Ncap if N is None else N
-    if P.dim() == 2:
-        _need(P, "P", torch.float32, 2)
-        L = P.shape[0]
-        sPb = sPh = 0
-        if P.stride(0) != D:
-            raise ValueError("P rows must be contiguous")
-    else:
-        _need(P, "P", torch.float32, 4)
-        L = P.shape[2]
-        sPb, sPh = P.stride(0), P.stride(1)
-        if P.stride(2) != D:
-            raise ValueError("P rows must be contiguous")
+    L, sPb, sPh = _proj(P, D)
     if codes_out is None:
         codes_out = torch.zeros(B, Hkv, Ncap, max(1, L // 32), dtype=torch.int32, device=K.device)
     _u32_codes(codes_out, "codes_out")
@@ -203,8 +214,8 @@ def decode_attention(q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, codes: t
     """One BinaryPC decode step; returns out [B, Hq, 128] fp32.
 
     q [B, Hq, 128] bf16 contiguous; K, V [B, Hkv, >=N, 128] bf16; codes
-    int32 storage [B, Hkv, >=N, L/32]; P [B, Hkv, L, 128] fp32 (or shared
-    [L, 128]).  Optional debug outputs: idx_out [B, Hkv, k] int32,
+    int32 storage [B, Hkv, >=N, L/32]; P [B, Hkv, L, 128] fp32, or shared
+    across the batch as [Hkv, L, 128] (offline calibration) or [L, 128].  Optional debug outputs: idx_out [B, Hkv, k] int32,
     score_out [B, Hkv, N] int32, qcode_out [B, Hkv, 8, L/32] int32.
     `events`: BPC_DECODE_STAGES + 1 torch.cuda.Event objects recorded at the
     stage boundaries (for measurement).
@@ -222,12 +233,7 @@ def decode_attention(q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, codes: t
     _, Hkv, Ncap, _ = K.shape
     N = Ncap if N is None else N
     _u32_codes(codes)
-    if P.dim() == 2:
-        L = P.shape[0]
-        sPb = sPh = 0
-    else:
-        L = P.shape[2]
-        sPb, sPh = P.stride(0), P.stride(1)
+    L, sPb, sPh = _proj(P, D)
     if sm_scale is None:
         sm_scale = 1.0 / math.sqrt(D)
     if out is None:
@@ -281,3 +287,27 @@ def select_hard(err: torch.Tensor, m: int, N: Optional[int] = None, *, serr_out:
                                 _stream(stream)),
            "bpc_select_hard")
     return serr_out
+
+
+def append_kv(k_new: torch.Tensor, v_new: torch.Tensor, K: torch.Tensor, V: torch.Tensor, codes: torch.Tensor,
+              P: torch.Tensor, pos: int, *, err_out: Optional[torch.Tensor] = None,
+              fragile: Optional[torch.Tensor] = None, stream=None) -> None:
+    """Decode-time append: store k_new, v_new [B, Hkv, T, 128] bf16 at rows
+    [pos, pos + T) of the caches K, V [B, Hkv, Ncap, 128] and their codes
+    (Algorithm 2 against P, [B, Hkv, L, 128] or a shared [L, 128]) at the same
+    rows of codes [B, Hkv, Ncap, L/32]."""
+    for t, nm in ((k_new, "k_new"), (v_new, "v_new"), (K, "K"), (V, "V")):
+        _need(t, nm, torch.bfloat16, 4)
+    B, Hkv, T, D = k_new.shape
+    if tuple(v_new.shape) != (B, Hkv, T, D):
+        raise ValueError("v_new must have the shape of k_new")
+    Ncap = K.shape[2]
+    if tuple(K.shape[:2]) != (B, Hkv) or tuple(V.shape[:3]) != (B, Hkv, Ncap):
+        raise ValueError("K and V must be [B, Hkv, Ncap, D] with the batch and heads of k_new")
+    _u32_codes(codes)
+    L, sPb, sPh = _proj(P, D)
+    _check(_lib.bpc_append_kv(_ptr(k_new), *_kv_strides(k_new), _ptr(v_new), *_kv_strides(v_new), _ptr(K),
+                              *_kv_strides(K), _ptr(V), *_kv_strides(V), _ptr(codes), codes.stride(0),
+                              codes.stride(1), _ptr(P), sPb, sPh, B, Hkv, Ncap, pos, T, D, L, _ptr(err_out),
+                              _ptr(fragile), _stream(stream)),
+           "bpc_append_kv")

@@ -186,6 +186,36 @@ int bpc_hash_keys(const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t sK_n, i
   return BPC_OK;
 }
 
+int bpc_append_kv(const uint16_t* k_new, int64_t sKn_b, int64_t sKn_h, int64_t sKn_t, const uint16_t* v_new,
+                  int64_t sVn_b, int64_t sVn_h, int64_t sVn_t, uint16_t* K, int64_t sK_b, int64_t sK_h,
+                  int64_t sK_n, uint16_t* V, int64_t sV_b, int64_t sV_h, int64_t sV_n, uint32_t* codes,
+                  int64_t sC_b, int64_t sC_h, const float* P, int64_t sP_b, int64_t sP_h, int B, int Hkv,
+                  int Ncap, int pos, int T, int D, int L, float* err_out, unsigned long long* fragile_out,
+                  void* stream) {
+  g_last_error[0] = 0;
+  int st;
+  if ((st = check_sizes(B, Hkv, Ncap))) return st;
+  if (T < 1 || pos < 0 || (int64_t)pos + T > Ncap)
+    return fail(BPC_EINVAL, "pos=%d, T=%d must satisfy pos >= 0, T >= 1, pos + T <= Ncap=%d", pos, T, Ncap);
+  if ((st = check_head_dim(D))) return st;
+  if ((st = check_code_len(L))) return st;
+  if ((st = check_kv("k_new", k_new, sKn_b, sKn_h, sKn_t))) return st;
+  if ((st = check_kv("v_new", v_new, sVn_b, sVn_h, sVn_t))) return st;
+  if ((st = check_kv("K", K, sK_b, sK_h, sK_n))) return st;
+  if ((st = check_kv("V", V, sV_b, sV_h, sV_n))) return st;
+  if ((st = check_proj(P, sP_b, sP_h))) return st;
+  if ((st = check_codes("codes", codes, sC_b, sC_h, L / 32))) return st;
+  if ((st = check_opt_aligned("err_out", err_out))) return st;
+  AppendCopy cp{};
+  cp.Kc = K + (int64_t)pos * sK_n, cp.sKc_b = sK_b, cp.sKc_h = sK_h, cp.sKc_n = sK_n;
+  cp.Vn = v_new, cp.sVn_b = sVn_b, cp.sVn_h = sVn_h, cp.sVn_n = sVn_t;
+  cp.Vc = V + (int64_t)pos * sV_n, cp.sVc_b = sV_b, cp.sVc_h = sV_h, cp.sVc_n = sV_n;
+  hipError_t e = launch_hash(k_new, sKn_b, sKn_h, sKn_t, B, Hkv, T, L, P, sP_b, sP_h, codes + (int64_t)pos * (L / 32),
+                             sC_b, sC_h, err_out, fragile_out, static_cast<hipStream_t>(stream), &cp);
+  if (e != hipSuccess) return hip_fail(e, "bpc_append_kv launch");
+  return BPC_OK;
+}
+
 size_t bpc_decode_workspace_bytes(int B, int Hq, int Hkv, int N, int D, int L, int k) {
   if (B < 1 || Hkv < 1 || Hq < Hkv || Hq % Hkv || N < 1 || k < 1 || k > N || D != kHeadDim) return 0;
   if (L != 32 && L != 64 && L != 128) return 0;

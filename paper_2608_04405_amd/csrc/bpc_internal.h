@@ -106,10 +106,21 @@ hipError_t launch_decode(const DecodeArgs& a);
 hipError_t launch_select_hard(const float* err, int64_t sE_b, int64_t sE_h, int B, int Hkv, int N, int m,
                               int32_t* out, hipStream_t stream);
 
+// Decode-time append: the cache rows the new keys and values are copied to
+// (pointers already at the first new position).
+struct AppendCopy {
+  uint16_t* Kc;
+  int64_t sKc_b, sKc_h, sKc_n;
+  const uint16_t* Vn;
+  int64_t sVn_b, sVn_h, sVn_n;
+  uint16_t* Vc;
+  int64_t sVc_b, sVc_h, sVc_n;
+};
+
 hipError_t launch_hash(const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t sK_n, int B, int Hkv,
                        int N, int L, const float* P, int64_t sP_b, int64_t sP_h, uint32_t* codes,
                        int64_t sC_b, int64_t sC_h, float* err, unsigned long long* fragile,
-                       hipStream_t stream);
+                       hipStream_t stream, const AppendCopy* append = nullptr);
 
 hipError_t launch_build(const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t sK_n, int B, int Hkv,
                         int N, int L, const float* G, float* P, uint32_t* codes, int64_t sC_b,

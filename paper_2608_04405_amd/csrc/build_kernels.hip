@@ -197,12 +197,16 @@ hipError_t launch_build(const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t s
 // workgroup (padded rows avoid bank conflicts between the four blocks).
 // ============================================================================
 
+// With a cache copy (cp.Kc non-null), decode-time append: each key row of K
+// (the new keys) is also stored into the cache rows cp.Kc, and the matching
+// value rows cp.Vn into cp.Vc; the four lanes of a key each move a quarter
+// of both rows.
 template <int L>
 __global__ __launch_bounds__(256) void hash_kernel(const uint16_t* __restrict__ K, int64_t sK_b, int64_t sK_h,
                                                    int64_t sK_n, int Hkv, int N, const float* __restrict__ P,
                                                    int64_t sP_b, int64_t sP_h, uint32_t* __restrict__ codes,
                                                    int64_t sC_b, int64_t sC_h, float* __restrict__ err,
-                                                   unsigned long long* __restrict__ fragile) {
+                                                   unsigned long long* __restrict__ fragile, AppendCopy cp) {
   constexpr int W = L / 32;
   constexpr int PAD = 33;
   __shared__ float p_s[L][4][PAD];
@@ -223,13 +227,25 @@ __global__ __launch_bounds__(256) void hash_kernel(const uint16_t* __restrict__ 
   double r[32];
   if (valid) {
     const uint16_t* krow = K + b * sK_b + h * sK_h + (int64_t)key * sK_n + 32 * qd;
+    uint4 kq[4];
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
       const uint4 v = *reinterpret_cast<const uint4*>(krow + 8 * c);
+      kq[c] = v;
       const uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
       for (int e = 0; e < 8; ++e)
         r[8 * c + e] = bf16_to_f64((uint16_t)((e & 1) ? (w[e >> 1] >> 16) : (w[e >> 1] & 0xFFFFu)));
+    }
+    if (cp.Kc) {
+      uint16_t* kc = cp.Kc + b * cp.sKc_b + h * cp.sKc_h + (int64_t)key * cp.sKc_n + 32 * qd;
+      const uint16_t* vn = cp.Vn + b * cp.sVn_b + h * cp.sVn_h + (int64_t)key * cp.sVn_n + 32 * qd;
+      uint16_t* vc = cp.Vc + b * cp.sVc_b + h * cp.sVc_h + (int64_t)key * cp.sVc_n + 32 * qd;
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        reinterpret_cast<uint4*>(kc)[c] = kq[c];
+        reinterpret_cast<uint4*>(vc)[c] = reinterpret_cast<const uint4*>(vn)[c];
+      }
     }
   } else {
 #pragma unroll
@@ -273,20 +289,21 @@ __global__ __launch_bounds__(256) void hash_kernel(const uint16_t* __restrict__ 
 
 hipError_t launch_hash(const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t sK_n, int B, int Hkv, int N, int L,
                        const float* P, int64_t sP_b, int64_t sP_h, uint32_t* codes, int64_t sC_b, int64_t sC_h,
-                       float* err, unsigned long long* fragile, hipStream_t stream) {
+                       float* err, unsigned long long* fragile, hipStream_t stream, const AppendCopy* append) {
   const dim3 grid((N + 63) / 64, B * Hkv);
+  const AppendCopy cp = append ? *append : AppendCopy{};
   switch (L) {
     case 32:
       hash_kernel<32><<<grid, 256, 0, stream>>>(K, sK_b, sK_h, sK_n, Hkv, N, P, sP_b, sP_h, codes, sC_b, sC_h, err,
-                                                fragile);
+                                                fragile, cp);
       break;
     case 64:
       hash_kernel<64><<<grid, 256, 0, stream>>>(K, sK_b, sK_h, sK_n, Hkv, N, P, sP_b, sP_h, codes, sC_b, sC_h, err,
-                                                fragile);
+                                                fragile, cp);
       break;
     default:
       hash_kernel<128><<<grid, 256, 0, stream>>>(K, sK_b, sK_h, sK_n, Hkv, N, P, sP_b, sP_h, codes, sC_b, sC_h,
-                                                 err, fragile);
+                                                 err, fragile, cp);
       break;
   }
   return hipGetLastError();

@@ -220,3 +220,40 @@ def _decode_eas(lib, **kw):
 def test_decode_eas_rejects(lib, kw, code):
     assert _decode_eas(lib, **kw) == code
     assert lib.bpc_last_error() != b""
+
+
+def _append(lib, **kw):
+    a = dict(kn=FAKE, sKnb=8 * 128, sKnh=128, sKnt=128, vn=FAKE, sVnb=8 * 128, sVnh=128, sVnt=128, K=FAKE,
+             sKb=8 * 4096 * 128, sKh=4096 * 128, sKn=128, V=FAKE, sVb=8 * 4096 * 128, sVh=4096 * 128, sVn=128,
+             codes=FAKE, sCb=8 * 4096 * 2, sCh=4096 * 2, P=FAKE, sPb=8 * 64 * 128, sPh=64 * 128, B=1, Hkv=8,
+             Ncap=4096, pos=4095, T=1, D=128, L=64, err=None, frag=None, stream=None)
+    a.update(kw)
+    f = lib.bpc_append_kv
+    f.restype = ctypes.c_int
+    v = ctypes.c_void_p
+    return f(v(a["kn"]), _i64(a["sKnb"]), _i64(a["sKnh"]), _i64(a["sKnt"]), v(a["vn"]), _i64(a["sVnb"]),
+             _i64(a["sVnh"]), _i64(a["sVnt"]), v(a["K"]), _i64(a["sKb"]), _i64(a["sKh"]), _i64(a["sKn"]), v(a["V"]),
+             _i64(a["sVb"]), _i64(a["sVh"]), _i64(a["sVn"]), v(a["codes"]), _i64(a["sCb"]), _i64(a["sCh"]),
+             v(a["P"]), _i64(a["sPb"]), _i64(a["sPh"]), a["B"], a["Hkv"], a["Ncap"], a["pos"], a["T"], a["D"],
+             a["L"], v(a["err"]), v(a["frag"]), v(a["stream"]))
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(pos=4096), EINVAL),        # past the cache
+    (dict(pos=4090, T=7), EINVAL),
+    (dict(pos=-1), EINVAL),
+    (dict(T=0), EINVAL),
+    (dict(kn=None), EINVAL),
+    (dict(vn=None), EINVAL),
+    (dict(V=None), EINVAL),
+    (dict(codes=None), EINVAL),
+    (dict(P=None), EINVAL),
+    (dict(D=64), EUNSUP),
+    (dict(L=16), EUNSUP),
+    (dict(sCh=4097), EALIGN),        # not a multiple of the code words
+    (dict(kn=FAKE + 8), EALIGN),
+    (dict(err=FAKE + 4), EALIGN),
+])
+def test_append_rejects(lib, kw, code):
+    assert _append(lib, **kw) == code
+    assert lib.bpc_last_error() != b""

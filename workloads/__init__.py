@@ -9,6 +9,7 @@ from .synth import (  # noqa: F401
     CONFIGS,
     DecodeConfig,
     config_by_name,
+    make_calibration_keys,
     make_gaussian_directions,
     make_layer,
 )

@@ -224,3 +224,20 @@ def make_layer(cfg: DecodeConfig, layer: int = 0, device="cpu",
             pos[b, h] = ph
         del Kh, Vh
     return {"q": q, "K": K, "V": V, "G": make_gaussian_directions(cfg), "needle_pos": pos}
+
+
+def make_calibration_keys(cfg: DecodeConfig, layer: int = 0, n_seq: int = 4, device="cpu") -> torch.Tensor:
+    """Keys of n_seq held-out sequences of the same layer (sequence indices
+    B .. B + n_seq - 1, so they share the layer's key basis but none of the
+    batch's keys, and carry no needles), concatenated per KV head:
+    [1, Hkv, n_seq * N, D] bf16.  They stand in for the calibration corpus
+    of offline projection calibration."""
+    c = cfg.replace(needles=0)
+    K = torch.zeros(1, c.Hkv, n_seq * c.N, c.D, dtype=torch.bfloat16, device=device)
+    q = torch.zeros(c.B + n_seq, c.Hq, c.D, dtype=torch.bfloat16, device=device)  # unused without needles
+    for h in range(c.Hkv):
+        basis = _key_basis(c, layer, h, device)
+        for i in range(n_seq):
+            Kh, _, _ = make_head(c, q, layer, c.B + i, h, device, basis=basis)
+            K[0, h, i * c.N:(i + 1) * c.N] = Kh
+    return K
