@@ -297,6 +297,29 @@ def main():
                    "reconstruction error, chosen per (b, h) at prefill by select_hard)"}
     log(f"safeguard: {eas}")
 
+    # ---------------------------------------------------------------- dense decode attention (context)
+    # full attention over all 131072 keys of every (b, h): what the sparse
+    # step replaces (the paper quotes its speed-ups against dense attention)
+    ws_dense = torch.empty(int(bpc._lib.bpc_dense_workspace_bytes(B, Hq, Hkv, N, D)), dtype=torch.uint8, device=dev)
+    for j in range(3):
+        it = insts[j % len(insts)]
+        bpc.dense_attention(it["q"], it["K"], it["V"], sm, out=outs[j % len(insts)], workspace=ws_dense)
+    dense_steps = 10
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for j in range(dense_steps):
+        it = insts[j % len(insts)]
+        bpc.dense_attention(it["q"], it["K"], it["V"], sm, out=outs[j % len(insts)], workspace=ws_dense)
+    e1.record()
+    torch.cuda.synchronize()
+    dense_us = e0.elapsed_time(e1) / dense_steps * 1e3
+    dense_bytes = B * Hkv * N * 2 * D * 2 + B * Hq * D * (2 + 4)
+    dense = {"us_per_step": round(dense_us, 1), "GBps": round(dense_bytes / (dense_us * 1e-6) / 1e9, 1),
+             "sparse_speedup": round(dense_us / (ms_per_step * 1e3), 2),
+             "what": "dense decode attention over all keys (every K and V row read), the comparison point"}
+    del ws_dense
+    log(f"dense: {dense}")
+
     # ---------------------------------------------------------------- offline projection calibration (context)
     # one P per KV head built offline (Algorithm 1 over held-out keys), then
     # the batch's prefill is Algorithm 2 against it and decode reads it with
@@ -381,6 +404,7 @@ def main():
         "roofline": roofline,
         "prefill": prefill,
         "eas": eas,
+        "dense": dense,
         "opc": opc,
         "cpu_baseline": cpu,
         "wall_s_timed": round(wall, 4),

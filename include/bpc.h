@@ -269,6 +269,26 @@ int bpc_decode_attention_eas(const uint16_t* q,
                              void* stream);
 
 /*
+ * bpc_dense_attention -- dense decode attention over all N cached keys
+ * (softmax of (q_g . K_n) * sm_scale over n = 0..N-1, applied to V; fp32
+ * accumulation).  Not part of the method: it is the comparison point the
+ * paper's efficiency results are quoted against (full attention at decode,
+ * Sec. 4.2 "Efficiency Evaluation"), provided for measuring the sparse step
+ * against.  Arguments as for bpc_decode_attention; the workspace holds the
+ * per-chunk partials, bpc_dense_workspace_bytes(...) bytes, 256-byte aligned.
+ * Cost: two kernel launches.
+ */
+size_t bpc_dense_workspace_bytes(int B, int Hq, int Hkv, int N, int D);
+int bpc_dense_attention(const uint16_t* q,
+                        const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t sK_n,
+                        const uint16_t* V, int64_t sV_b, int64_t sV_h, int64_t sV_n,
+                        int B, int Hq, int Hkv, int N, int D,
+                        float sm_scale,
+                        float* out,
+                        void* workspace, size_t workspace_bytes,
+                        void* stream);
+
+/*
  * bpc_decode_attention_profiled -- bpc_decode_attention that also records
  * caller-created hipEvent_t handles on `stream` at the stage boundaries
  * (query packing | scoring | threshold, selection and attention | merge):

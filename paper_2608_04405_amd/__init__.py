@@ -25,6 +25,7 @@ __all__ = [
     "hash_keys",
     "decode_attention",
     "decode_workspace_bytes",
+    "dense_attention",
     "select_hard",
     "DECODE_STAGES",
     "DECODE_STAGE_NAMES",
@@ -66,6 +67,11 @@ _lib.bpc_decode_attention_eas.argtypes = [_p, _p, _i64, _i64, _i64, _p, _i64, _i
 _lib.bpc_append_kv.restype = _i
 _lib.bpc_append_kv.argtypes = [_p, _i64, _i64, _i64, _p, _i64, _i64, _i64, _p, _i64, _i64, _i64, _p, _i64, _i64, _i64,
                                _p, _i64, _i64, _p, _i64, _i64, _i, _i, _i, _i, _i, _i, _i, _p, _p, _p]
+_lib.bpc_dense_workspace_bytes.restype = _sz
+_lib.bpc_dense_workspace_bytes.argtypes = [_i, _i, _i, _i, _i]
+_lib.bpc_dense_attention.restype = _i
+_lib.bpc_dense_attention.argtypes = [_p, _p, _i64, _i64, _i64, _p, _i64, _i64, _i64, _i, _i, _i, _i, _i,
+                                     ctypes.c_float, _p, _p, _sz, _p]
 _lib.bpc_select_hard.restype = _i
 _lib.bpc_select_hard.argtypes = [_p, _i64, _i64, _i, _i, _i, _i, _p, _p]
 _lib.bpc_decode_attention_profiled.restype = _i
@@ -311,3 +317,29 @@ def append_kv(k_new: torch.Tensor, v_new: torch.Tensor, K: torch.Tensor, V: torc
                               codes.stride(1), _ptr(P), sPb, sPh, B, Hkv, Ncap, pos, T, D, L, _ptr(err_out),
                               _ptr(fragile), _stream(stream)),
            "bpc_append_kv")
+
+
+def dense_attention(q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, sm_scale: Optional[float] = None,
+                    N: Optional[int] = None, *, out: Optional[torch.Tensor] = None,
+                    workspace: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """Dense decode attention over all N cached keys (the comparison point
+    for the sparse step); returns out [B, Hq, 128] fp32."""
+    _need(q, "q", torch.bfloat16, 3)
+    _need(K, "K", torch.bfloat16, 4)
+    _need(V, "V", torch.bfloat16, 4)
+    if not q.is_contiguous():
+        raise ValueError("q must be contiguous")
+    B, Hq, D = q.shape
+    _, Hkv, Ncap, _ = K.shape
+    N = Ncap if N is None else N
+    if sm_scale is None:
+        sm_scale = 1.0 / math.sqrt(D)
+    if out is None:
+        out = torch.empty(B, Hq, D, dtype=torch.float32, device=q.device)
+    need = int(_lib.bpc_dense_workspace_bytes(B, Hq, Hkv, N, D))
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=q.device)
+    _check(_lib.bpc_dense_attention(_ptr(q), _ptr(K), *_kv_strides(K), _ptr(V), *_kv_strides(V), B, Hq, Hkv, N, D,
+                                    float(sm_scale), _ptr(out), _ptr(workspace), workspace.numel(), _stream(stream)),
+           "bpc_dense_attention")
+    return out

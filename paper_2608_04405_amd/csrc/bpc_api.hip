@@ -312,6 +312,51 @@ int bpc_decode_attention_eas(const uint16_t* q, const uint16_t* K, int64_t sK_b,
                      workspace_bytes, stream, nullptr, 0);
 }
 
+size_t bpc_dense_workspace_bytes(int B, int Hq, int Hkv, int N, int D) {
+  if (B < 1 || Hkv < 1 || Hq < Hkv || Hq % Hkv || N < 1 || D != kHeadDim) return 0;
+  const size_t nchunks = ((size_t)N + kSlice - 1) / kSlice;
+  return align_up((size_t)B * Hkv * nchunks * (Hq / Hkv) * (kHeadDim + 2) * sizeof(float), 256);
+}
+
+int bpc_dense_attention(const uint16_t* q, const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t sK_n,
+                        const uint16_t* V, int64_t sV_b, int64_t sV_h, int64_t sV_n, int B, int Hq, int Hkv, int N,
+                        int D, float sm_scale, float* out, void* workspace, size_t workspace_bytes, void* stream) {
+  g_last_error[0] = 0;
+  int st;
+  if ((st = check_sizes(B, Hkv, N))) return st;
+  if (Hq < Hkv || Hq % Hkv) return fail(BPC_EINVAL, "Hq=%d must be a positive multiple of Hkv=%d", Hq, Hkv);
+  {
+    const int G = Hq / Hkv;
+    if (G > kMaxGroup || (G & (G - 1)))
+      return fail(BPC_EUNSUPPORTED, "group size Hq/Hkv=%d must be 1, 2, 4, 8 or 16", G);
+  }
+  if ((st = check_head_dim(D))) return st;
+  if ((int64_t)N > (int64_t)kMaxSlices * kSlice)
+    return fail(BPC_EUNSUPPORTED, "N=%d: at most %d cached keys per head", N, kMaxSlices * kSlice);
+  if (!(sm_scale > 0.0f) || !__builtin_isfinite(sm_scale))
+    return fail(BPC_EINVAL, "sm_scale must be finite and > 0");
+  if (!q || !out) return fail(BPC_EINVAL, "q and out are required");
+  if (!aligned16(q) || !aligned16(out)) return fail(BPC_EALIGN, "q and out must be 16-byte aligned");
+  if ((st = check_kv("K", K, sK_b, sK_h, sK_n))) return st;
+  if ((st = check_kv("V", V, sV_b, sV_h, sV_n))) return st;
+  if ((int64_t)(N - 1) * sK_n * 2 + 256 > (int64_t)UINT32_MAX || (int64_t)(N - 1) * sV_n * 2 + 256 > (int64_t)UINT32_MAX)
+    return fail(BPC_EUNSUPPORTED, "the N rows of one head must span less than 4 GiB");
+  const size_t need = bpc_dense_workspace_bytes(B, Hq, Hkv, N, D);
+  if (!workspace || workspace_bytes < need)
+    return fail(BPC_EWORKSPACE, "workspace of %zu bytes given, %zu needed", workspace ? workspace_bytes : 0, need);
+  if (reinterpret_cast<uintptr_t>(workspace) & 255u) return fail(BPC_EALIGN, "workspace must be 256-byte aligned");
+  DenseArgs a{};
+  a.q = q;
+  a.K = K, a.sK_b = sK_b, a.sK_h = sK_h, a.sK_n = sK_n;
+  a.V = V, a.sV_b = sV_b, a.sV_h = sV_h, a.sV_n = sV_n;
+  a.B = B, a.Hq = Hq, a.Hkv = Hkv, a.N = N, a.sm_scale = sm_scale, a.out = out;
+  a.ws = static_cast<char*>(workspace);
+  a.stream = static_cast<hipStream_t>(stream);
+  hipError_t e = launch_dense(a);
+  if (e != hipSuccess) return hip_fail(e, "bpc_dense_attention launch");
+  return BPC_OK;
+}
+
 int bpc_select_hard(const float* err, int64_t sE_b, int64_t sE_h, int B, int Hkv, int N, int m, int32_t* serr_out,
                     void* stream) {
   g_last_error[0] = 0;

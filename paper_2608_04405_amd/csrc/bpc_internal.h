@@ -103,6 +103,21 @@ struct DecodeArgs {
 
 hipError_t launch_decode(const DecodeArgs& a);
 
+// dense decode attention (full softmax over all N keys), the comparison point
+struct DenseArgs {
+  const uint16_t* q;
+  const uint16_t* K;
+  int64_t sK_b, sK_h, sK_n;
+  const uint16_t* V;
+  int64_t sV_b, sV_h, sV_n;
+  int B, Hq, Hkv, N;
+  float sm_scale;
+  float* out;
+  char* ws;  // partials: B Hkv ceil(N / kSlice) (Hq / Hkv) (128 + 2) fp32
+  hipStream_t stream;
+};
+hipError_t launch_dense(const DenseArgs& a);
+
 hipError_t launch_select_hard(const float* err, int64_t sE_b, int64_t sE_h, int B, int Hkv, int N, int m,
                               int32_t* out, hipStream_t stream);
 

@@ -757,6 +757,55 @@ __device__ __forceinline__ void attend_pass(int myidx, int nrows, const uint4 (*
   }
 }
 
+// The workgroup's partial for each query head g: each wavefront reduces its
+// weighted V over its four row groups; the wavefronts are combined under
+// their common maximum into pb[g] = (max, sum, o[128]) (base-2 logits).
+// o_s and st_s are LDS arrays; the caller ensures o_s is free to write.
+template <int G>
+__device__ __forceinline__ void write_partial(float (&o_s)[kAttnWaves][G][kHeadDim], float (&st_s)[kAttnWaves][G][2],
+                                              const float (&Mx)[G], const float (&Ls)[G], float (&o)[G][8],
+                                              float* __restrict__ pb) {
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, l16 = lane & 15;
+#pragma unroll
+  for (int g = 0; g < G; ++g)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      float x = o[g][e];
+      x += __shfl_xor(x, 16, 64);
+      x += __shfl_xor(x, 32, 64);
+      o[g][e] = x;
+    }
+  if (lane < 16) {
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o_s[wid][g][8 * l16 + e] = o[g][e];
+  }
+  if (lane == 0) {
+#pragma unroll
+    for (int g = 0; g < G; ++g) st_s[wid][g][0] = Mx[g], st_s[wid][g][1] = Ls[g];
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < G * (kHeadDim + 2); e += kAttnThreads) {
+    const int g = e / (kHeadDim + 2), d = e % (kHeadDim + 2);
+    float m = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < kAttnWaves; ++w) m = fmaxf(m, st_s[w][g][0]);
+    float acc = 0.f;
+    if (d == 0) {
+      acc = m;
+    } else {
+#pragma unroll
+      for (int w = 0; w < kAttnWaves; ++w) {
+        const float mw = st_s[w][g][0];
+        const float f = (mw == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mw - m);
+        acc = fmaf(d == 1 ? st_s[w][g][1] : o_s[w][g][d - 2], f, acc);
+      }
+    }
+    pb[e] = acc;
+  }
+}
+
 template <int G>
 __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(G <= 4 ? 4 : 1))) void attend_kernel(
     int N, int k, int L, int BH, int Hkv, int nslices, int win_ok, const uint32_t* __restrict__ cand,
@@ -1169,48 +1218,54 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(G 
   BPC_NOTE(2, 14, planned);
   __syncthreads();  // the row list is read to the end before its area holds o
 
-  // ---- the slice's partial: each wavefront reduces o over its four row
-  // groups; the wavefronts are combined under their common maximum
-#pragma unroll
-  for (int g = 0; g < G; ++g)
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      float x = o[g][e];
-      x += __shfl_xor(x, 16, 64);
-      x += __shfl_xor(x, 32, 64);
-      o[g][e] = x;
-    }
-  if (lane < 16) {
-#pragma unroll
-    for (int g = 0; g < G; ++g)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) sh.u.o[wid][g][8 * l16 + e] = o[g][e];
-  }
-  if (lane == 0) {
-#pragma unroll
-    for (int g = 0; g < G; ++g) sh.st[wid][g][0] = Mx[g], sh.st[wid][g][1] = Ls[g];
+  write_partial<G>(sh.u.o, sh.st, Mx, Ls, o, part + sl * G * (kHeadDim + 2));
+  BPC_STAMP(2, 6);
+}
+
+// ---------------------------------------------------------------------------
+// Dense decode attention over all N keys: the comparison point the paper's
+// efficiency numbers are quoted against (full attention at decode), not part
+// of the method.  One 256-thread workgroup per chunk of kSlice consecutive
+// keys of a (b, h); each wavefront takes runs of 16 consecutive rows with the
+// same row pass as the sparse kernel; the partials go through merge_kernel.
+// ---------------------------------------------------------------------------
+template <int G>
+struct DenseShared {
+  float o[kAttnWaves][G][kHeadDim];
+  float st[kAttnWaves][G][2];
+  uint4 q[G][kHeadDim / 8];
+};
+
+template <int G>
+__global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(G <= 4 ? 4 : 1))) void dense_kernel(
+    int N, int Hkv, int nchunks, const uint16_t* __restrict__ q, const uint16_t* __restrict__ K, int64_t sK_b,
+    int64_t sK_h, int64_t sK_n, const uint16_t* __restrict__ V, int64_t sV_b, int64_t sV_h, int64_t sV_n,
+    float scale_log2, float* __restrict__ part) {
+  __shared__ DenseShared<G> sh;
+  const int bh = blockIdx.x / nchunks, s = blockIdx.x % nchunks;
+  const int b = bh / Hkv, h = bh % Hkv;
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  if (threadIdx.x < G * kHeadDim / 8) {
+    const uint4* qb = reinterpret_cast<const uint4*>(q + ((size_t)b * Hkv * G + (size_t)h * G) * kHeadDim);
+    sh.q[threadIdx.x / (kHeadDim / 8)][threadIdx.x % (kHeadDim / 8)] = qb[threadIdx.x];
   }
   __syncthreads();
-  float* pb = part + sl * G * (kHeadDim + 2);
-  for (int e = threadIdx.x; e < G * (kHeadDim + 2); e += kAttnThreads) {
-    const int g = e / (kHeadDim + 2), d = e % (kHeadDim + 2);
-    float m = -INFINITY;
+  const int n0 = s * kSlice, cnt = min(kSlice, N - n0);
+  const char* Kh = reinterpret_cast<const char*>(K + b * sK_b + h * sK_h);
+  const char* Vh = reinterpret_cast<const char*>(V + b * sV_b + h * sV_h);
+  const uint32_t kstride = (uint32_t)sK_n * 2u, vstride = (uint32_t)sV_n * 2u;
+  float Mx[G], Ls[G], o[G][8];
 #pragma unroll
-    for (int w = 0; w < kAttnWaves; ++w) m = fmaxf(m, sh.st[w][g][0]);
-    float acc = 0.f;
-    if (d == 0) {
-      acc = m;
-    } else {
+  for (int g = 0; g < G; ++g) {
+    Mx[g] = -INFINITY, Ls[g] = 0.f;
 #pragma unroll
-      for (int w = 0; w < kAttnWaves; ++w) {
-        const float mw = sh.st[w][g][0];
-        const float f = (mw == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mw - m);
-        acc = fmaf(d == 1 ? sh.st[w][g][1] : sh.u.o[w][g][d - 2], f, acc);
-      }
-    }
-    pb[e] = acc;
+    for (int e = 0; e < 8; ++e) o[g][e] = 0.f;
   }
-  BPC_STAMP(2, 6);
+  for (int r0 = wid * kAttnRows; r0 < cnt; r0 += kAttnWaves * kAttnRows) {
+    const int nr = min(kAttnRows, cnt - r0);
+    attend_pass<G>(lane < nr ? n0 + r0 + lane : 0, nr, sh.q, Kh, kstride, Vh, vstride, scale_log2, Mx, Ls, o);
+  }
+  write_partial<G>(sh.o, sh.st, Mx, Ls, o, part + (size_t)blockIdx.x * G * (kHeadDim + 2));
 }
 
 // ---------------------------------------------------------------------------
@@ -1323,6 +1378,31 @@ extern "C" int bpc_trace_buffer(void* buf) {
   return hipMemcpyToSymbol(HIP_SYMBOL(g_trace), &buf, sizeof(buf)) == hipSuccess ? 0 : -1;
 }
 #endif
+
+hipError_t launch_dense(const DenseArgs& a) {
+  const int BH = a.B * a.Hkv, G = a.Hq / a.Hkv;
+  const int nchunks = (a.N + kSlice - 1) / kSlice;
+  const int nwg = BH * nchunks;
+  float* part = reinterpret_cast<float*>(a.ws);
+  const float scale_log2 = a.sm_scale * 1.4426950408889634f;
+  switch (G) {
+#define BPC_DENSE_CASE(GG)                                                                                         \
+  case GG:                                                                                                         \
+    dense_kernel<GG><<<nwg, kAttnThreads, 0, a.stream>>>(a.N, a.Hkv, nchunks, a.q, a.K, a.sK_b, a.sK_h, a.sK_n, a.V, \
+                                                         a.sV_b, a.sV_h, a.sV_n, scale_log2, part);               \
+    break;
+    BPC_DENSE_CASE(1)
+    BPC_DENSE_CASE(2)
+    BPC_DENSE_CASE(4)
+    BPC_DENSE_CASE(8)
+    BPC_DENSE_CASE(16)
+#undef BPC_DENSE_CASE
+    default:
+      break;
+  }
+  merge_kernel<<<a.B * a.Hq, kHeadDim, 0, a.stream>>>(a.Hkv, G, nchunks, part, a.out);
+  return hipGetLastError();
+}
 
 hipError_t launch_decode(const DecodeArgs& a) {
   const DecodeLayout lay = decode_layout(a.B, a.Hq, a.Hkv, a.N, a.L, a.k);

@@ -257,3 +257,24 @@ def _append(lib, **kw):
 def test_append_rejects(lib, kw, code):
     assert _append(lib, **kw) == code
     assert lib.bpc_last_error() != b""
+
+
+def test_dense_workspace_and_rejects(lib):
+    ws = lib.bpc_dense_workspace_bytes
+    ws.restype = ctypes.c_size_t
+    assert ws(16, 32, 8, 131072, 128) == 16 * 8 * 8 * 4 * 130 * 4
+    assert ws(1, 8, 8, 4096, 64) == 0
+    f = lib.bpc_dense_attention
+    f.restype = ctypes.c_int
+
+    def call(**kw):
+        a = dict(q=FAKE, K=FAKE, V=FAKE, B=1, Hq=8, Hkv=8, N=4096, D=128, sm=0.088, out=FAKE, ws=FAKE, wsb=0)
+        a.update(kw)
+        v = ctypes.c_void_p
+        return f(v(a["q"]), v(a["K"]), _i64(8 * 4096 * 128), _i64(4096 * 128), _i64(128), v(a["V"]),
+                 _i64(8 * 4096 * 128), _i64(4096 * 128), _i64(128), a["B"], a["Hq"], a["Hkv"], a["N"], a["D"],
+                 ctypes.c_float(a["sm"]), v(a["out"]), v(a["ws"]), ctypes.c_size_t(a["wsb"]), None)
+
+    for kw, code in ((dict(q=None), EINVAL), (dict(Hq=12), EINVAL), (dict(Hq=24), EUNSUP), (dict(D=64), EUNSUP),
+                     (dict(sm=0.0), EINVAL), (dict(K=FAKE + 2), EALIGN), (dict(wsb=16), EWS)):
+        assert call(**kw) == code, kw
