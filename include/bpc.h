@@ -99,7 +99,11 @@ int bpc_version(void);
  *           decisions is ADDED (the caller zeroes it), or NULL
  * workspace    device memory of at least bpc_build_workspace_bytes(...)
  *           bytes, 256-byte aligned; its contents on entry do not matter.
- * Cost: 3 L + 1 kernel launches; the fp64 residual lives in the workspace.
+ * Cost: 2 L + 2 kernel launches.  Nothing of size N x D is stored: each
+ * bit's pass recomputes R_j from the bf16 key, the key's code bits so far
+ * and P (the same rounded subtractions, in the same order), so the
+ * workspace holds one fp64 partial sum per 128-key chunk and coordinate
+ * plus fp64 copies of P and G.
  */
 size_t bpc_build_workspace_bytes(int B, int Hkv, int N, int D, int L);
 int bpc_build_hash(const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t sK_n,

@@ -97,15 +97,16 @@ DecodeLayout decode_layout(int B, int Hq, int Hkv, int N, int L, int k) {
 }
 
 BuildLayout build_layout(int B, int Hkv, int N, int L) {
-  (void)L;
   BuildLayout b{};
   const size_t BH = (size_t)B * Hkv;
-  b.nchunks = (N + kBuildRows - 1) / kBuildRows;
+  b.nchunks = (N + kBuildChunk - 1) / kBuildChunk;
   size_t o = 0;
-  b.off_R = o;
-  o = align_up(o + BH * kHeadDim * (size_t)N * sizeof(double), 256);
-  b.off_part = o;
+  b.off_part = o;  // one fp64 tree sum per chunk and coordinate
   o = align_up(o + BH * b.nchunks * (size_t)kHeadDim * sizeof(double), 256);
+  b.off_p64 = o;   // P widened to fp64, the scalar operand of the residual
+  o = align_up(o + BH * (size_t)L * kHeadDim * sizeof(double), 256);
+  b.off_g64 = o;   // G widened to fp64
+  o = align_up(o + (size_t)L * kHeadDim * sizeof(double), 256);
   b.total = o;
   return b;
 }

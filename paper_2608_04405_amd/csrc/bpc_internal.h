@@ -49,7 +49,9 @@ constexpr int kWinRec = 4 + kWinBins / 2;  // u32 per record
 constexpr int kWinSlices = 64;             // slices per (b, h) the one-round threshold handles
 
 // ---- build tiling ----------------------------------------------------------
-constexpr int kBuildRows = 256;  // rows per workgroup in the build passes
+constexpr int kBuildGroups = 2;                  // groups of 64 keys per build workgroup
+constexpr int kBuildThreads = 256 * kBuildGroups;  // four wavefronts (coordinate blocks) per group
+constexpr int kBuildChunk = 64 * kBuildGroups;     // keys per workgroup (one chunk of the row tree)
 
 // ---- workspace layouts -----------------------------------------------------
 // Decode, per slice sl = (b Hkv + h) nslices + s: candidates [kSlice] u32
@@ -69,7 +71,7 @@ struct DecodeLayout {
 
 struct BuildLayout {
   int nchunks;
-  size_t off_R, off_part, total;
+  size_t off_part, off_p64, off_g64, total;
 };
 
 DecodeLayout decode_layout(int B, int Hq, int Hkv, int N, int L, int k);

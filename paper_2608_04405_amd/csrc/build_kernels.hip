@@ -13,177 +13,285 @@
 namespace bpc {
 
 // ============================================================================
-// Algorithm 1.  The fp64 residual R of every (sequence, KV head) lives in
-// the workspace in dimension-major layout [bh][d][n], so that a wavefront
-// whose lanes own consecutive keys reads one coalesced 512-byte line per d.
-// One bit costs three launches:
-//   build_dot      per key: apply the previous bit's update, store R, a = R_j . g_i,
-//                  u_j = sign(a), write code bit i
-//   build_reduce   per 256-key chunk: pairwise tree of u_j R_j over the chunk
-//   build_finish   per (b, h): pairwise tree over chunks, v = s / N, P[i] = (float)v
-// A final build_dot pass (bit == L) applies the last update and writes ||R_j||.
-// The chunk trees are full binary trees over 256 rows padded with +0, so
-// chunk tree + chunk-sum tree equals the pairwise tree over all N rows
-// (padding only changes the sign of zero sums).
+// Algorithm 1.  Each bit is one pass over the keys of every (sequence, KV
+// head) plus one reduction per (b, h):
+//   build_bit_kernel    one workgroup per chunk of kBuildChunk keys, in groups
+//                       of 64 (one key per lane); the four wavefronts of a
+//                       group own the coordinate blocks [32 c, 32 c + 32), so
+//                       every lane of a wavefront needs the same element of P
+//                       and G at the same time and reads it as a scalar
+//                       operand.  The fp64 residual of the lane's key is
+//                       recomputed from the bf16 key, the key's code bits
+//                       decided so far and the stored rows of P,
+//                       R = (((k - u_0 P_0) - u_1 P_1) - ...), one rounded
+//                       subtraction per bit (fma(-u, p, r) with u = +-1 is that
+//                       subtraction: the product is exact), exactly as an
+//                       in-place update would compute it.  Then a_j = R_j . g_i
+//                       (fixed order), u_j and code bit i, and the chunk's
+//                       pairwise tree of u_j R_j: a full binary tree over its
+//                       rows, +0 past N, formed across lanes by a reduce-scatter
+//                       butterfly (each level halves the coordinates a lane
+//                       carries) and across the key groups in LDS.
+//   build_finish_kernel pairwise tree over the chunk sums, v = s / N,
+//                       P[i] = (float)v (and its fp64 widening for the next
+//                       passes).
+// A final build_bit pass (bit == L) recomputes the last residual and writes
+// ||R_j||.  Nothing of size N x D is stored: the pass reads the keys again,
+// trading fp64 arithmetic (about L^2 D / 2 fused subtractions per key over the
+// whole build) for memory traffic.
 // ============================================================================
 
-__global__ __launch_bounds__(kBuildRows) void build_dot_kernel(
+// the partner lane's value at lane ^ M (quad permutes for 1 and 2)
+template <int M>
+__device__ __forceinline__ double xor_lane(double x) {
+  if constexpr (M == 1 || M == 2) {
+    constexpr int ctrl = (M == 1) ? 0xB1 : 0x4E;  // quad_perm [1,0,3,2] / [2,3,0,1]
+    const int lo = __builtin_amdgcn_mov_dpp(__double2loint(x), ctrl, 0xF, 0xF, false);
+    const int hi = __builtin_amdgcn_mov_dpp(__double2hiint(x), ctrl, 0xF, 0xF, false);
+    return __hiloint2double(hi, lo);
+  } else {
+    return __shfl_xor(x, M, 64);
+  }
+}
+
+// A wavefront-uniform address of data that no kernel writes while this one
+// runs, in the constant address space so that loads through it are scalar.
+template <typename T>
+using const_ptr = const __attribute__((address_space(4))) T*;
+
+template <typename T>
+__device__ __forceinline__ const_ptr<T> uniform_ptr(const T* p) {
+  const uint64_t a = reinterpret_cast<uint64_t>(p);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)a);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(a >> 32));
+  return (const_ptr<T>)(((uint64_t)hi << 32) | lo);
+}
+
+// one reduce-scatter level: lanes l and l ^ (1 << K) add their halves of the
+// 2 * HALF coordinates they carry; the lane with bit K clear keeps the lower half
+template <int K, int HALF>
+__device__ __forceinline__ void rs_level(double (&v)[32], int lane) {
+  const bool upper = (lane >> K) & 1;
+#pragma unroll
+  for (int e = 0; e < HALF; ++e) {
+    const double send = upper ? v[e] : v[HALF + e];
+    const double keep = upper ? v[HALF + e] : v[e];
+    v[e] = dadd(keep, xor_lane<1 << K>(send));
+  }
+}
+
+__global__ void build_prep_kernel(const float* __restrict__ G, double* __restrict__ G64, int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) G64[i] = (double)G[i];
+}
+
+template <int W>
+__global__ __launch_bounds__(kBuildThreads) void build_bit_kernel(
     const uint16_t* __restrict__ K, int64_t sK_b, int64_t sK_h, int64_t sK_n, int Hkv, int N, int L, int bit,
-    const float* __restrict__ G, const float* __restrict__ P, uint32_t* __restrict__ codes, int64_t sC_b,
-    int64_t sC_h, double* __restrict__ R, float* __restrict__ err, unsigned long long* __restrict__ fragile) {
+    const double* __restrict__ G64, const double* __restrict__ P64, uint32_t* __restrict__ codes, int64_t sC_b,
+    int64_t sC_h, double* __restrict__ part, int nchunks, float* __restrict__ err,
+    unsigned long long* __restrict__ fragile) {
+  __shared__ double xch[kBuildGroups][4][64];         // per-block partial dots of each key
+  __shared__ double groot[kBuildGroups][kHeadDim];    // tree root of each key group
+  __shared__ int frag;
   const int bh = blockIdx.y;
   const int b = bh / Hkv, h = bh % Hkv;
-  const int W = L >> 5;
-  const int j = blockIdx.x * kBuildRows + threadIdx.x;
-  __shared__ double g_s[kHeadDim];
-  __shared__ double p_s[kHeadDim];
-  __shared__ int frag_s;
+  const int lane = threadIdx.x & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int c = wv & 3, grp = wv >> 2;
   const bool final_pass = (bit == L);
-  if (threadIdx.x < kHeadDim) {
-    if (!final_pass) g_s[threadIdx.x] = (double)G[(size_t)bit * kHeadDim + threadIdx.x];
-    if (bit > 0) p_s[threadIdx.x] = (double)P[((size_t)bh * L + (bit - 1)) * kHeadDim + threadIdx.x];
-  }
-  if (threadIdx.x == 0) frag_s = 0;
-  __syncthreads();
+  if (threadIdx.x == 0) frag = 0;
 
-  int is_fragile = 0;
-  if (j < N) {
-    uint32_t* crow = codes + b * sC_b + h * sC_h + (int64_t)j * W;
-    bool up = false;
-    if (bit > 0) up = (crow[(bit - 1) >> 5] >> ((bit - 1) & 31)) & 1u;
-    double* Rj = R + (size_t)bh * kHeadDim * N + j;
-    double acc[4] = {0.0, 0.0, 0.0, 0.0};
-    if (bit == 0) {
-      const uint16_t* krow = K + b * sK_b + h * sK_h + (int64_t)j * sK_n;
+  const int key = blockIdx.x * kBuildChunk + grp * 64 + lane;
+  const bool valid = key < N;
+  double r[32];
+  uint32_t cw[W];
 #pragma unroll
-      for (int c = 0; c < kHeadDim / 8; ++c) {
-        const uint4 v = *reinterpret_cast<const uint4*>(krow + 8 * c);
-        const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+  for (int w = 0; w < W; ++w) cw[w] = 0u;
+  uint32_t* crow = codes + b * sC_b + h * sC_h + (int64_t)(valid ? key : 0) * W;
+  if (valid) {
+    const uint16_t* krow = K + b * sK_b + h * sK_h + (int64_t)key * sK_n + 32 * c;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const int d = 8 * c + e;
-          const uint16_t kb = (uint16_t)((e & 1) ? (w[e >> 1] >> 16) : (w[e >> 1] & 0xFFFFu));
-          const double r = bf16_to_f64(kb);
-          Rj[(size_t)d * N] = r;
-          acc[d >> 5] = dadd(acc[d >> 5], dmul(r, g_s[d]));
-        }
-      }
-    } else {
-#pragma unroll 8
-      for (int d = 0; d < kHeadDim; ++d) {
-        const double pv = p_s[d];
-        double r = Rj[(size_t)d * N];
-        r = r - (up ? pv : -pv);
-        if (final_pass) {
-          acc[d >> 5] = dadd(acc[d >> 5], dmul(r, r));
-        } else {
-          Rj[(size_t)d * N] = r;
-          acc[d >> 5] = dadd(acc[d >> 5], dmul(r, g_s[d]));
-        }
-      }
+    for (int q = 0; q < 4; ++q) {
+      const uint4 v = *reinterpret_cast<const uint4*>(krow + 8 * q);
+      const uint32_t wd[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        r[8 * q + e] = bf16_to_f64((uint16_t)((e & 1) ? (wd[e >> 1] >> 16) : (wd[e >> 1] & 0xFFFFu)));
     }
-    const double a = dadd(dadd(acc[0], acc[1]), dadd(acc[2], acc[3]));
-    if (final_pass) {
-      if (err) err[(size_t)bh * N + j] = (float)sqrt(a);
-    } else {
-      const uint32_t ubit = (a >= 0.0) ? 1u : 0u;
-      is_fragile = fragile_decision(a) ? 1 : 0;
-      uint32_t* wp = crow + (bit >> 5);
-      const uint32_t prev = (bit & 31) ? *wp : 0u;
-      *wp = prev | (ubit << (bit & 31));
+#pragma unroll
+    for (int w = 0; w < W; ++w)
+      if (32 * w < bit) cw[w] = crow[w];
+  } else {
+#pragma unroll
+    for (int e = 0; e < 32; ++e) r[e] = 0.0;  // never contributes: padded below
+  }
+  // the residual after bits 0 .. bit - 1
+  const_ptr<double> prow = uniform_ptr(P64 + (size_t)bh * L * kHeadDim + 32 * c);
+#pragma unroll
+  for (int w = 0; w < W; ++w) {
+    const int nb = min(32, bit - 32 * w);
+    const uint32_t word = cw[w];
+    for (int ib = 0; ib < nb; ++ib) {
+      const double sg = ((word >> ib) & 1u) ? -1.0 : 1.0;
+      const_ptr<double> p = prow + (size_t)(32 * w + ib) * kHeadDim;
+#pragma unroll
+      for (int e = 0; e < 32; ++e) r[e] = __builtin_fma(sg, p[e], r[e]);
     }
   }
-  if (fragile && !final_pass) {
-    const unsigned long long m = __ballot(is_fragile);
-    if ((threadIdx.x & 63) == 0 && m) atomicAdd(&frag_s, __popcll(m));
+  if (final_pass) {
+    double sq = 0.0;
+#pragma unroll
+    for (int e = 0; e < 32; ++e) sq = dadd(sq, dmul(r[e], r[e]));
+    xch[grp][c][lane] = sq;
     __syncthreads();
-    if (threadIdx.x == 0 && frag_s) atomicAdd(fragile, (unsigned long long)frag_s);
+    if (err && c == 0 && valid)
+      err[(size_t)bh * N + key] = (float)sqrt(dadd(dadd(xch[grp][0][lane], xch[grp][1][lane]),
+                                                   dadd(xch[grp][2][lane], xch[grp][3][lane])));
+    return;
   }
-}
-
-__global__ __launch_bounds__(kBuildRows) void build_reduce_kernel(const uint32_t* __restrict__ codes,
-                                                                 int64_t sC_b, int64_t sC_h, int Hkv, int N,
-                                                                 int L, int bit, const double* __restrict__ R,
-                                                                 double* __restrict__ part) {
-  const int bh = blockIdx.y;
-  const int b = bh / Hkv, h = bh % Hkv;
-  const int W = L >> 5;
-  const int chunk = blockIdx.x;
-  const int row0 = chunk * kBuildRows;
-  __shared__ double u_s[kBuildRows];
-  {
-    const int j = row0 + threadIdx.x;
-    double u = 0.0;
-    if (j < N) {
-      const uint32_t w = codes[b * sC_b + h * sC_h + (int64_t)j * W + (bit >> 5)];
-      u = ((w >> (bit & 31)) & 1u) ? 1.0 : -1.0;
+  // a_j = R_j . g (four blocks of 32, ascending, combined ((b0 + b1) + (b2 + b3)))
+  const_ptr<double> g = uniform_ptr(G64 + (size_t)bit * kHeadDim + 32 * c);
+  double acc = 0.0;
+#pragma unroll
+  for (int e = 0; e < 32; ++e) acc = dadd(acc, dmul(r[e], g[e]));
+  xch[grp][c][lane] = acc;
+  __syncthreads();
+  const double a =
+      dadd(dadd(xch[grp][0][lane], xch[grp][1][lane]), dadd(xch[grp][2][lane], xch[grp][3][lane]));
+  const bool u = a >= 0.0;
+  if (c == 0) {
+    if (valid) crow[bit >> 5] = ((bit & 31) ? cw[bit >> 5] : 0u) | ((u ? 1u : 0u) << (bit & 31));
+    if (fragile) {
+      const unsigned long long m = __ballot(valid && fragile_decision(a));
+      if (lane == 0 && m) atomicAdd(&frag, __popcll(m));
     }
-    u_s[threadIdx.x] = u;
+  }
+  // u_j R_j (exact), keys past N padded with +0, and the tree over the
+  // group's 64 keys: after the five reduce-scatter levels lane l carries the
+  // coordinate whose index is l's low five bits reversed, summed over its
+  // half of the group; the xor-32 step adds the two halves
+  double v[32];
+#pragma unroll
+  for (int e = 0; e < 32; ++e) v[e] = valid ? (u ? r[e] : -r[e]) : 0.0;
+  rs_level<0, 16>(v, lane);
+  rs_level<1, 8>(v, lane);
+  rs_level<2, 4>(v, lane);
+  rs_level<3, 2>(v, lane);
+  rs_level<4, 1>(v, lane);
+  const double s = dadd(v[0], xor_lane<32>(v[0]));
+  if (lane < 32) {
+    const int e = (int)(__brev((uint32_t)lane) >> 27);
+    groot[grp][32 * c + e] = s;
   }
   __syncthreads();
-  const int lane32 = threadIdx.x & 31;
-  const int dsub = threadIdx.x >> 5;  // 0..7
-  const double* Rb = R + (size_t)bh * kHeadDim * N;
-  for (int dg = 0; dg < kHeadDim / 8; ++dg) {
-    const int d = dg * 8 + dsub;
-    const double* Rd = Rb + (size_t)d * N + row0 + lane32 * 8;
-    double v[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int j = row0 + lane32 * 8 + e;
-      v[e] = (j < N) ? u_s[lane32 * 8 + e] * Rd[e] : 0.0;
-    }
-    double s = dadd(dadd(dadd(v[0], v[1]), dadd(v[2], v[3])), dadd(dadd(v[4], v[5]), dadd(v[6], v[7])));
-    // pairwise across the 32 lanes of this d: partner sums are added as (mine + theirs),
-    // which equals (left + right) because IEEE addition is commutative
-#pragma unroll
-    for (int m = 1; m < 32; m <<= 1) s = dadd(s, __shfl_xor(s, m, 64));
-    if (lane32 == 0) part[((size_t)bh * gridDim.x + chunk) * kHeadDim + d] = s;
-  }
+  static_assert(kBuildGroups == 2, "one tree level across the key groups");
+  if (threadIdx.x < kHeadDim)
+    part[((size_t)bh * nchunks + blockIdx.x) * kHeadDim + threadIdx.x] =
+        dadd(groot[0][threadIdx.x], groot[1][threadIdx.x]);
+  if (fragile && threadIdx.x == 0 && frag) atomicAdd(fragile, (unsigned long long)frag);
 }
 
-__global__ __launch_bounds__(kHeadDim) void build_finish_kernel(int N, int L, int bit, int nchunks,
-                                                               const double* __restrict__ part,
-                                                               float* __restrict__ P) {
+// One workgroup per (b, h): thread (blk, d) folds an aligned block of S
+// chunk sums of coordinate d (S a power of two, 8 blocks cover all chunks) as
+// a binary counter, and the block roots are then paired level by level in LDS
+// with the odd one carried.  Both are the pairwise tree with the odd element
+// carried: a binary counter's final right fold equals level-wise pairing, and
+// level-wise pairing of the leaves splits at every aligned power of two.
+constexpr int kFinishBlocks = 8;
+
+__global__ __launch_bounds__(kFinishBlocks* kHeadDim) void build_finish_kernel(int N, int L, int bit, int nchunks,
+                                                                               const double* __restrict__ part,
+                                                                               float* __restrict__ P,
+                                                                               double* __restrict__ P64) {
+  __shared__ double node[kFinishBlocks][kHeadDim];
   const int bh = blockIdx.x;
-  const int d = threadIdx.x;
-  // pairwise tree with the odd element carried, evaluated as a binary
-  // counter: a completed subtree of level l merges with the pending subtree
-  // of the same level, and what remains is combined from the smallest up
+  const int d = threadIdx.x & (kHeadDim - 1), blk = threadIdx.x >> 7;
+  int S = 1;
+  while (S * kFinishBlocks < nchunks) S <<= 1;
+  const int begin = blk * S, end = min(begin + S, nchunks);
+  const double* src = part + (size_t)bh * nchunks * kHeadDim + d;
   double stack_v[32];
   int stack_l[32];
   int top = 0;
-  for (int c = 0; c < nchunks; ++c) {
-    double x = part[((size_t)bh * nchunks + c) * kHeadDim + d];
-    int lvl = 0;
-    while (top > 0 && stack_l[top - 1] == lvl) {
-      x = dadd(stack_v[top - 1], x);
-      --top;
-      ++lvl;
+  for (int c0 = begin; c0 < end; c0 += 8) {
+    double x[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) x[e] = (c0 + e < end) ? src[(size_t)(c0 + e) * kHeadDim] : 0.0;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      if (c0 + e >= end) break;
+      double y = x[e];
+      int lvl = 0;
+      while (top > 0 && stack_l[top - 1] == lvl) {
+        y = dadd(stack_v[top - 1], y);
+        --top;
+        ++lvl;
+      }
+      stack_v[top] = y;
+      stack_l[top] = lvl;
+      ++top;
     }
-    stack_v[top] = x;
-    stack_l[top] = lvl;
-    ++top;
   }
-  double s = stack_v[top - 1];
-  for (int t = top - 2; t >= 0; --t) s = dadd(stack_v[t], s);
-  const double v = s / (double)N;
-  P[((size_t)bh * L + bit) * kHeadDim + d] = (float)v;
+  if (top > 0) {
+    double y = stack_v[top - 1];
+    for (int t = top - 2; t >= 0; --t) y = dadd(stack_v[t], y);
+    node[blk][d] = y;
+  }
+  int cnt = (nchunks + S - 1) / S;
+  while (cnt > 1) {
+    __syncthreads();
+    const int half = (cnt + 1) >> 1;
+    double y = 0.0;
+    if (blk < half) y = (2 * blk + 1 < cnt) ? dadd(node[2 * blk][d], node[2 * blk + 1][d]) : node[2 * blk][d];
+    __syncthreads();
+    if (blk < half) node[blk][d] = y;
+    cnt = half;
+  }
+  if (blk == 0) {
+    const double v = node[0][d] / (double)N;
+    const float pf = (float)v;
+    P[((size_t)bh * L + bit) * kHeadDim + d] = pf;
+    P64[((size_t)bh * L + bit) * kHeadDim + d] = (double)pf;
+  }
+}
+
+template <int W>
+static void launch_build_W(const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t sK_n, int B, int Hkv, int N,
+                           int L, const double* G64, float* P, double* P64, uint32_t* codes, int64_t sC_b,
+                           int64_t sC_h, float* err, unsigned long long* fragile, double* part, int nchunks,
+                           hipStream_t stream) {
+  const dim3 grid(nchunks, B * Hkv);
+  for (int bit = 0; bit <= L; ++bit) {
+    build_bit_kernel<W><<<grid, kBuildThreads, 0, stream>>>(K, sK_b, sK_h, sK_n, Hkv, N, L, bit, G64, P64, codes,
+                                                           sC_b, sC_h, part, nchunks, err, fragile);
+    if (bit == L) break;
+    build_finish_kernel<<<B * Hkv, kFinishBlocks * kHeadDim, 0, stream>>>(N, L, bit, nchunks, part, P, P64);
+  }
 }
 
 hipError_t launch_build(const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t sK_n, int B, int Hkv, int N,
                         int L, const float* G, float* P, uint32_t* codes, int64_t sC_b, int64_t sC_h,
                         float* err, unsigned long long* fragile, char* ws, hipStream_t stream) {
   const BuildLayout lay = build_layout(B, Hkv, N, L);
-  double* R = reinterpret_cast<double*>(ws + lay.off_R);
   double* part = reinterpret_cast<double*>(ws + lay.off_part);
-  const dim3 grid(lay.nchunks, B * Hkv);
-  for (int bit = 0; bit <= L; ++bit) {
-    build_dot_kernel<<<grid, kBuildRows, 0, stream>>>(K, sK_b, sK_h, sK_n, Hkv, N, L, bit, G, P, codes, sC_b, sC_h,
-                                                      R, err, fragile);
-    if (bit == L) break;
-    build_reduce_kernel<<<grid, kBuildRows, 0, stream>>>(codes, sC_b, sC_h, Hkv, N, L, bit, R, part);
-    build_finish_kernel<<<B * Hkv, kHeadDim, 0, stream>>>(N, L, bit, lay.nchunks, part, P);
+  double* P64 = reinterpret_cast<double*>(ws + lay.off_p64);
+  double* G64 = reinterpret_cast<double*>(ws + lay.off_g64);
+  const int ng = L * kHeadDim;
+  build_prep_kernel<<<(ng + 255) / 256, 256, 0, stream>>>(G, G64, ng);
+  switch (L) {
+    case 32:
+      launch_build_W<1>(K, sK_b, sK_h, sK_n, B, Hkv, N, L, G64, P, P64, codes, sC_b, sC_h, err, fragile, part,
+                        lay.nchunks, stream);
+      break;
+    case 64:
+      launch_build_W<2>(K, sK_b, sK_h, sK_n, B, Hkv, N, L, G64, P, P64, codes, sC_b, sC_h, err, fragile, part,
+                        lay.nchunks, stream);
+      break;
+    default:
+      launch_build_W<4>(K, sK_b, sK_h, sK_n, B, Hkv, N, L, G64, P, P64, codes, sC_b, sC_h, err, fragile, part,
+                        lay.nchunks, stream);
+      break;
   }
   return hipGetLastError();
 }
