@@ -56,6 +56,7 @@ __all__ = [
     "select_hard",
     "eas_budget",
     "decode_head_eas",
+    "decode_per_query_head",
     "budget_keys",
     "FRAGILE_THRESHOLD",
 ]
@@ -382,6 +383,20 @@ def decode_head(q_bits, K_bits, V_bits, codes, P, k: int, sm_scale: float):
     idx = select_topk(c, k)
     out = attend(q_bits, K_bits, V_bits, idx, sm_scale)
     return {"p": qq["p"], "qcode": qq["qcode"], "T": qq["T"], "scores": c, "idx": idx, "out": out}
+
+
+def decode_per_query_head(q_bits, K_bits, V_bits, codes, P, k: int, sm_scale: float):
+    """Per-query-head selection, the alternative to one selection per KV
+    head: every query head g of the group projects and quantises its own
+    query q_g P^T (Sec. 3.2 "Retrieval Phase"), scores every cached code of
+    the shared KV head against it (Alg. 3), takes its own top-k and attends
+    over its own selection.  q_bits [Gq, D]; returns per-head stacks:
+    p [Gq, L], qcode [Gq, 8, L/32], scores [Gq, N], idx [Gq, k], out [Gq, D]."""
+    q_bits = np.asarray(q_bits)
+    heads = [decode_head(q_bits[g:g + 1], K_bits, V_bits, codes, P, k, sm_scale) for g in range(q_bits.shape[0])]
+    return {"p": np.stack([r["p"] for r in heads]), "qcode": np.stack([r["qcode"] for r in heads]),
+            "scores": np.stack([r["scores"] for r in heads]), "idx": np.stack([r["idx"] for r in heads]),
+            "out": np.concatenate([r["out"] for r in heads], axis=0)}
 
 
 # --------------------------------------------------------------------------

@@ -568,4 +568,50 @@ def pin_eas_union(o):
     assert np.allclose(r["out"], o.full_attention(q, K, V, sm), rtol=1e-12, atol=1e-13)
 
 
+def pin_per_query_head(o):
+    """Per-query-head selection against facts that fix it without retyping it:
+    opposite queries give exactly negated scores (while the group rule sees a
+    zero sum and ties everything), identical queries reproduce the group rule
+    (the quantisation is scale invariant for a power-of-two group), a head's
+    result does not depend on the other heads' queries, and G = 1 is the
+    ordinary decode step."""
+    rng = np.random.default_rng(31)
+    N, D, L, k = 600, 128, 64, 25
+    K = random_bf16(rng, (N, D))
+    V = random_bf16(rng, (N, D))
+    codes = rng.integers(0, 1 << 32, size=(N, L // 32), dtype=np.uint64).astype(np.uint32)
+    P = (0.5 * rng.standard_normal((L, D))).astype(np.float32)
+    sm = 1.0 / np.sqrt(D)
+    q0 = random_bf16(rng, (1, D))
+    # opposite heads: q1 = -q0 exactly (bf16 negation flips the sign bit)
+    q = np.concatenate([q0, q0 ^ np.uint16(0x8000)])
+    r = o.decode_per_query_head(q, K, V, codes, P, k, sm)
+    assert np.array_equal(r["scores"][1], -r["scores"][0])
+    assert np.array_equal(r["p"][1], -r["p"][0])
+    grp = o.decode_head(q, K, V, codes, P, k, sm)
+    assert np.all(grp["scores"] == 0) and np.array_equal(grp["idx"], np.arange(k))
+    H = o.unpack_codes(codes, L).astype(np.int64)
+    best0 = np.lexsort((np.arange(N), -(H @ r["p"][0])))[:k]
+    assert np.array_equal(r["idx"][0], np.sort(best0))
+    for g in range(2):
+        logits = bf16_values(q[g]) @ bf16_values(K[r["idx"][g]]).T * sm
+        w = torch.softmax(torch.from_numpy(logits), dim=0).numpy()
+        assert np.allclose(r["out"][g], w @ bf16_values(V[r["idx"][g]]), rtol=1e-12, atol=1e-13)
+    # identical heads (G = 4): every head selects what the group selects
+    q4 = np.repeat(q0, 4, axis=0)
+    r4 = o.decode_per_query_head(q4, K, V, codes, P, k, sm)
+    g4 = o.decode_head(q4, K, V, codes, P, k, sm)
+    for g in range(4):
+        assert np.array_equal(r4["idx"][g], g4["idx"]) and np.array_equal(r4["p"][g], g4["p"])
+    assert np.allclose(r4["out"], g4["out"], rtol=1e-12, atol=1e-13)
+    # a head ignores the other heads' queries; permuting heads permutes results
+    qa = random_bf16(rng, (3, D))
+    qb = qa.copy()
+    qb[1:] = random_bf16(rng, (2, D))
+    ra, rb = o.decode_per_query_head(qa, K, V, codes, P, k, sm), o.decode_per_query_head(qb, K, V, codes, P, k, sm)
+    assert np.array_equal(ra["idx"][0], rb["idx"][0]) and np.array_equal(ra["out"][0], rb["out"][0])
+    rp = o.decode_per_query_head(qa[::-1], K, V, codes, P, k, sm)
+    assert np.array_equal(rp["idx"], ra["idx"][::-1]) and np.array_equal(rp["qcode"], ra["qcode"][::-1])
+
+
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

@@ -48,6 +48,10 @@ MUTANTS = {
     "eas_intersection": ("union = np.union1d(idx, serr)", "union = np.intersect1d(idx, serr)"),
     "eas_added_inverted": ("added = (~np.isin(serr, idx)).astype(np.int32)", "added = np.isin(serr, idx).astype(np.int32)"),
     "eas_budget_floor": ("m = min(-(-budget * num // den), budget - 1)", "m = min(budget * num // den, budget - 1)"),
+    "perq_group_selection": ("heads = [decode_head(q_bits[g:g + 1], K_bits, V_bits, codes, P, k, sm_scale)",
+                             "heads = [decode_head(q_bits, K_bits, V_bits, codes, P, k, sm_scale)"),
+    "perq_first_head_only": ("heads = [decode_head(q_bits[g:g + 1], K_bits,", "heads = [decode_head(q_bits[0:1], K_bits,"),
+    "perq_head_order": ("for g in range(q_bits.shape[0])]", "for g in range(q_bits.shape[0])][::-1]"),
 }
 
 
