@@ -297,6 +297,48 @@ def main():
                    "reconstruction error, chosen per (b, h) at prefill by select_hard)"}
     log(f"safeguard: {eas}")
 
+    # ---------------------------------------------------------------- fixed-count budgets (context)
+    # the same step with k = 1024 and k = 2048 keys instead of 2 % of N
+    def timed(fn, nsteps):
+        for j in range(args.warmup):
+            fn(j)
+        ev[0].record()
+        for j in range(nsteps):
+            fn(j)
+        ev[1].record()
+        torch.cuda.synchronize()
+        return ev[0].elapsed_time(ev[1]) / nsteps * 1e3
+
+    fixed = {}
+    for kb in (1024, 2048):
+        ws_b = torch.empty(bpc.decode_workspace_bytes(B, Hq, Hkv, N, L, kb), dtype=torch.uint8, device=dev)
+
+        def fixed_step(j, kb=kb, ws_b=ws_b):
+            it = insts[j % len(insts)]
+            bpc.decode_attention(it["q"], it["K"], it["V"], it["codes"], it["P"], kb, sm, out=outs[j % len(insts)],
+                                 workspace=ws_b)
+
+        fixed[f"k{kb}_us_per_step"] = round(timed(fixed_step, max(10, min(args.steps, 100))), 2)
+        del ws_b
+    fixed["what"] = "the decode step with a fixed budget of 1024 or 2048 keys per (b, h)"
+    log(f"fixed budgets: {fixed}")
+
+    # ---------------------------------------------------------------- per-query-head selection (context)
+    ws_ph = torch.empty(bpc.decode_per_head_workspace_bytes(B, Hq, Hkv, N, L, k), dtype=torch.uint8, device=dev)
+
+    def per_head_step(j):
+        it = insts[j % len(insts)]
+        bpc.decode_attention_per_head(it["q"], it["K"], it["V"], it["codes"], it["P"], k, sm,
+                                      out=outs[j % len(insts)], workspace=ws_ph)
+
+    ph_us = timed(per_head_step, max(10, min(args.steps, 100)))
+    ph_bytes = B * Hq * N * W * 4 + B * Hq * k * 2 * D * 2 + B * Hq * L * D * 4 + B * Hq * D * (2 + 4)
+    per_head = {"us_per_step": round(ph_us, 2), "GBps": round(ph_bytes / (ph_us * 1e-6) / 1e9, 1),
+                "what": f"one selection of {k} keys per query head ({Hq // Hkv} scans of each KV head's codes and "
+                        f"{Hq // Hkv} gathers per (b, h))"}
+    del ws_ph
+    log(f"per query head: {per_head}")
+
     # ---------------------------------------------------------------- dense decode attention (context)
     # full attention over all 131072 keys of every (b, h): what the sparse
     # step replaces (the paper quotes its speed-ups against dense attention)
@@ -404,6 +446,8 @@ def main():
         "roofline": roofline,
         "prefill": prefill,
         "eas": eas,
+        "fixed_budget": fixed,
+        "per_query_head": per_head,
         "dense": dense,
         "opc": opc,
         "cpu_baseline": cpu,

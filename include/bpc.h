@@ -220,6 +220,43 @@ int bpc_decode_attention(const uint16_t* q,
                          void* stream);
 
 /*
+ * bpc_decode_attention_per_head -- the decode step with one selection per
+ * QUERY head instead of one per KV head (the alternative to the group rule
+ * of bpc_decode_attention; Sec. 3.2 "Retrieval Phase", Alg. 3, App. A.3
+ * "Scoring kernel", which scores query-key pairs head by head): query head j
+ * projects and quantises its own q_j P^T, scores every cached code of KV
+ * head floor(j / G) against it, takes its own top-k (ties to the lower
+ * index) and attends over its own selection.
+ *
+ * Arguments as for bpc_decode_attention, except:
+ * idx_out    [B, Hq, k] int32, ascending per query head (or NULL)
+ * score_out  [B, Hq, N] int32 (or NULL)
+ * qcode_out  [B, Hq, 8, L/32] uint32 (or NULL)
+ * workspace  at least bpc_decode_per_head_workspace_bytes(...) bytes,
+ *            256-byte aligned.
+ * Any power-of-two or other group size G = Hq / Hkv is accepted.
+ * Cost: the codes of a KV head are scanned once per query head (G times
+ * the code traffic of bpc_decode_attention) and G selections are gathered.
+ * When the batch stride of K, V, codes and P is Hkv times the head stride
+ * (contiguous heads) the batch is one launch sequence of four kernels;
+ * otherwise one per sequence.  Errors as for bpc_decode_attention.
+ */
+size_t bpc_decode_per_head_workspace_bytes(int B, int Hq, int Hkv, int N, int D, int L, int k);
+int bpc_decode_attention_per_head(const uint16_t* q,
+                                  const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t sK_n,
+                                  const uint16_t* V, int64_t sV_b, int64_t sV_h, int64_t sV_n,
+                                  const uint32_t* codes, int64_t sC_b, int64_t sC_h,
+                                  const float* P, int64_t sP_b, int64_t sP_h,
+                                  int B, int Hq, int Hkv, int N, int D, int L, int k,
+                                  float sm_scale,
+                                  float* out,
+                                  int32_t* idx_out,
+                                  int32_t* score_out,
+                                  uint32_t* qcode_out,
+                                  void* workspace, size_t workspace_bytes,
+                                  void* stream);
+
+/*
  * bpc_select_hard -- the hard-to-hash set of the Error-Aware Safeguard
  * (Sec. 3.2 "Error-Aware Safeguard (EAS)", Eq. reconstruction_error): for
  * every (b, KV head), the m keys with the largest reconstruction errors

@@ -25,6 +25,8 @@ __all__ = [
     "hash_keys",
     "decode_attention",
     "decode_workspace_bytes",
+    "decode_attention_per_head",
+    "decode_per_head_workspace_bytes",
     "dense_attention",
     "select_hard",
     "DECODE_STAGES",
@@ -60,6 +62,10 @@ _DECODE_ARGS = [_p, _p, _i64, _i64, _i64, _p, _i64, _i64, _i64, _p, _i64, _i64, 
                 _i, _i, _i, _i, _i, _i, _i, ctypes.c_float, _p, _p, _p, _p, _p, _sz, _p]
 _lib.bpc_decode_attention.restype = _i
 _lib.bpc_decode_attention.argtypes = _DECODE_ARGS
+_lib.bpc_decode_per_head_workspace_bytes.restype = _sz
+_lib.bpc_decode_per_head_workspace_bytes.argtypes = [_i, _i, _i, _i, _i, _i, _i]
+_lib.bpc_decode_attention_per_head.restype = _i
+_lib.bpc_decode_attention_per_head.argtypes = _DECODE_ARGS
 _lib.bpc_decode_attention_eas.restype = _i
 _lib.bpc_decode_attention_eas.argtypes = [_p, _p, _i64, _i64, _i64, _p, _i64, _i64, _i64, _p, _i64, _i64, _p, _i64, _i64,
                                           _i, _i, _i, _i, _i, _i, _i, ctypes.c_float, _p, _i64, _i64, _i, _p, _p, _p,
@@ -148,6 +154,10 @@ def build_workspace_bytes(B: int, Hkv: int, N: int, L: int, D: int = 128) -> int
 
 def decode_workspace_bytes(B: int, Hq: int, Hkv: int, N: int, L: int, k: int, D: int = 128) -> int:
     return int(_lib.bpc_decode_workspace_bytes(B, Hq, Hkv, N, D, L, k))
+
+
+def decode_per_head_workspace_bytes(B: int, Hq: int, Hkv: int, N: int, L: int, k: int, D: int = 128) -> int:
+    return int(_lib.bpc_decode_per_head_workspace_bytes(B, Hq, Hkv, N, D, L, k))
 
 
 def _u32_codes(codes: torch.Tensor, name: str = "codes") -> torch.Tensor:
@@ -276,6 +286,43 @@ def decode_attention(q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, codes: t
         _check(_lib.bpc_decode_attention_profiled(*args, handles, len(events)), "bpc_decode_attention_profiled")
     return out
 
+
+
+def decode_attention_per_head(q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, codes: torch.Tensor,
+                              P: torch.Tensor, k: int, sm_scale: Optional[float] = None, N: Optional[int] = None, *,
+                              out: Optional[torch.Tensor] = None, idx_out: Optional[torch.Tensor] = None,
+                              score_out: Optional[torch.Tensor] = None, qcode_out: Optional[torch.Tensor] = None,
+                              workspace: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """The decode step with one selection per query head: query head j
+    quantises its own projection, scores the codes of KV head j // G, takes
+    its own top-k and attends over it.  Shapes as decode_attention, except
+    idx_out [B, Hq, k], score_out [B, Hq, N], qcode_out [B, Hq, 8, L/32]."""
+    _need(q, "q", torch.bfloat16, 3)
+    _need(K, "K", torch.bfloat16, 4)
+    _need(V, "V", torch.bfloat16, 4)
+    if not q.is_contiguous():
+        raise ValueError("q must be contiguous")
+    B, Hq, D = q.shape
+    _, Hkv, Ncap, _ = K.shape
+    N = Ncap if N is None else N
+    _u32_codes(codes)
+    L, sPb, sPh = _proj(P, D)
+    if sm_scale is None:
+        sm_scale = 1.0 / math.sqrt(D)
+    if out is None:
+        out = torch.empty(B, Hq, D, dtype=torch.float32, device=q.device)
+    for t, name, shape in ((idx_out, "idx_out", (B, Hq, k)), (score_out, "score_out", (B, Hq, N)),
+                           (qcode_out, "qcode_out", (B, Hq, 8, L // 32))):
+        if t is not None and (t.dtype != torch.int32 or not t.is_contiguous() or tuple(t.shape) != shape):
+            raise ValueError(f"{name} must be a contiguous int32 tensor of shape {shape}")
+    ws_bytes = decode_per_head_workspace_bytes(B, Hq, Hkv, N, L, k, D)
+    if workspace is None:
+        workspace = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=q.device)
+    _check(_lib.bpc_decode_attention_per_head(
+        _ptr(q), _ptr(K), *_kv_strides(K), _ptr(V), *_kv_strides(V), _ptr(codes), codes.stride(0), codes.stride(1),
+        _ptr(P), sPb, sPh, B, Hq, Hkv, N, D, L, k, float(sm_scale), _ptr(out), _ptr(idx_out), _ptr(score_out),
+        _ptr(qcode_out), _ptr(workspace), workspace.numel(), _stream(stream)), "bpc_decode_attention_per_head")
+    return out
 
 def select_hard(err: torch.Tensor, m: int, N: Optional[int] = None, *, serr_out: Optional[torch.Tensor] = None,
                 stream=None) -> torch.Tensor:

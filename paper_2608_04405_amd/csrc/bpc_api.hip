@@ -313,6 +313,55 @@ int bpc_decode_attention_eas(const uint16_t* q, const uint16_t* K, int64_t sK_b,
                      workspace_bytes, stream, nullptr, 0);
 }
 
+size_t bpc_decode_per_head_workspace_bytes(int B, int Hq, int Hkv, int N, int D, int L, int k) {
+  if (B < 1 || Hkv < 1 || Hq < Hkv || Hq % Hkv || N < 1 || k < 1 || k > N || D != kHeadDim) return 0;
+  if (L != 32 && L != 64 && L != 128) return 0;
+  const int G = Hq / Hkv;
+  return decode_layout(B * Hkv, G, G, N, L, k).total;
+}
+
+// Per-query-head selection runs the decode path with one query per "KV
+// head": the G query heads of (b, h) become G heads of a sequence b' that
+// all read (b, h)'s K, V, codes and P (head stride 0).  When every tensor's
+// batch stride is Hkv times its head stride, b' = b Hkv + h addresses all
+// of them linearly and one call covers the batch; otherwise each sequence
+// is one call.
+int bpc_decode_attention_per_head(const uint16_t* q, const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t sK_n,
+                                  const uint16_t* V, int64_t sV_b, int64_t sV_h, int64_t sV_n,
+                                  const uint32_t* codes, int64_t sC_b, int64_t sC_h, const float* P, int64_t sP_b,
+                                  int64_t sP_h, int B, int Hq, int Hkv, int N, int D, int L, int k, float sm_scale,
+                                  float* out, int32_t* idx_out, int32_t* score_out, uint32_t* qcode_out,
+                                  void* workspace, size_t workspace_bytes, void* stream) {
+  g_last_error[0] = 0;
+  int st;
+  if ((st = check_sizes(B, Hkv, N))) return st;
+  if (Hq < Hkv || Hq % Hkv) return fail(BPC_EINVAL, "Hq=%d must be a positive multiple of Hkv=%d", Hq, Hkv);
+  if ((int64_t)B * Hkv > (int64_t)(1 << 20)) return fail(BPC_EINVAL, "B*Hkv=%lld too large", (long long)B * Hkv);
+  if ((st = check_kv("K", K, sK_b, sK_h, sK_n))) return st;
+  if ((st = check_kv("V", V, sV_b, sV_h, sV_n))) return st;
+  if ((st = check_code_len(L))) return st;
+  if ((st = check_codes("codes", codes, sC_b, sC_h, L / 32))) return st;
+  if ((st = check_proj(P, sP_b, sP_h))) return st;
+  const size_t need = bpc_decode_per_head_workspace_bytes(B, Hq, Hkv, N, D, L, k);
+  if (need && (!workspace || workspace_bytes < need))
+    return fail(BPC_EWORKSPACE, "workspace of %zu bytes given, %zu needed", workspace ? workspace_bytes : 0, need);
+  const int G = Hq / Hkv;
+  const bool linear = sK_b == Hkv * sK_h && sV_b == Hkv * sV_h && sC_b == Hkv * sC_h && sP_b == Hkv * sP_h;
+  const int calls = linear ? 1 : B;
+  const int Bc = linear ? B * Hkv : Hkv;  // sequences b' per call
+  const int W = L / 32;
+  for (int c = 0; c < calls; ++c) {
+    st = decode_impl(q + (size_t)c * Hq * kHeadDim, K + c * sK_b, sK_h, 0, sK_n, V + c * sV_b, sV_h, 0, sV_n,
+                     codes + c * sC_b, sC_h, 0, P + c * sP_b, sP_h, 0, Bc, G, G, N, D, L, k, sm_scale,
+                     out + (size_t)c * Hq * kHeadDim, idx_out ? idx_out + (size_t)c * Hq * k : nullptr,
+                     score_out ? score_out + (size_t)c * Hq * N : nullptr,
+                     qcode_out ? qcode_out + (size_t)c * Hq * 8 * W : nullptr, nullptr, 0, 0, 0, nullptr, workspace,
+                     workspace_bytes, stream, nullptr, 0);
+    if (st) return st;
+  }
+  return BPC_OK;
+}
+
 size_t bpc_dense_workspace_bytes(int B, int Hq, int Hkv, int N, int D) {
   if (B < 1 || Hkv < 1 || Hq < Hkv || Hq % Hkv || N < 1 || D != kHeadDim) return 0;
   const size_t nchunks = ((size_t)N + kSlice - 1) / kSlice;

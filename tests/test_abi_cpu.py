@@ -281,3 +281,33 @@ def test_dense_workspace_and_rejects(lib):
     for kw, code in ((dict(q=None), EINVAL), (dict(Hq=12), EINVAL), (dict(Hq=24), EUNSUP), (dict(D=64), EUNSUP),
                      (dict(sm=0.0), EINVAL), (dict(K=FAKE + 2), EALIGN), (dict(wsb=16), EWS)):
         assert call(**kw) == code, kw
+
+
+def test_per_head_workspace_and_rejects(lib):
+    ws = lib.bpc_decode_per_head_workspace_bytes
+    ws.restype = ctypes.c_size_t
+    assert ws(16, 32, 8, 131072, 128, 64, 2622) >= lib.bpc_decode_workspace_bytes(16, 32, 8, 131072, 128, 64, 2622)
+    assert ws(1, 8, 8, 4096, 64, 32, 82) == 0  # D != 128
+    assert ws(1, 12, 8, 4096, 128, 32, 82) == 0  # Hq % Hkv
+    f = lib.bpc_decode_attention_per_head
+    f.restype = ctypes.c_int
+
+    def call(**kw):
+        a = dict(q=FAKE, K=FAKE, sKb=8 * 4096 * 128, sKh=4096 * 128, sKn=128, V=FAKE, sVb=8 * 4096 * 128,
+                 sVh=4096 * 128, sVn=128, codes=FAKE, sCb=8 * 4096, sCh=4096, P=FAKE, sPb=8 * 32 * 128,
+                 sPh=32 * 128, B=1, Hq=32, Hkv=8, N=4096, D=128, L=32, k=82, sm=0.088, ws=FAKE, ws_bytes=0)
+        a.update(kw)
+        return f(ctypes.c_void_p(a["q"]), ctypes.c_void_p(a["K"]), _i64(a["sKb"]), _i64(a["sKh"]), _i64(a["sKn"]),
+                 ctypes.c_void_p(a["V"]), _i64(a["sVb"]), _i64(a["sVh"]), _i64(a["sVn"]),
+                 ctypes.c_void_p(a["codes"]), _i64(a["sCb"]), _i64(a["sCh"]), ctypes.c_void_p(a["P"]),
+                 _i64(a["sPb"]), _i64(a["sPh"]), a["B"], a["Hq"], a["Hkv"], a["N"], a["D"], a["L"], a["k"],
+                 ctypes.c_float(a["sm"]), ctypes.c_void_p(FAKE), None, None, None, ctypes.c_void_p(a["ws"]),
+                 ctypes.c_size_t(a["ws_bytes"]), None)
+
+    assert call(Hq=12) == EINVAL
+    assert call(K=None) == EINVAL
+    assert call(L=48) == EUNSUP
+    assert call(ws=None) == EWS
+    assert call(ws_bytes=1024) == EWS
+    assert call(k=0, ws_bytes=1 << 40) == EINVAL
+    assert call(D=64, ws_bytes=1 << 40) == EUNSUP

@@ -8,7 +8,8 @@ outputs that the oracle can afford, and through properties on every head.
   rebuilt by the oracle (projection and codes bit-exact) and decoded by the
   oracle (query planes, scores, indices bit-exact; output within 2e-3).
   The same head is then decoded with the error-aware safeguard (10 % of
-  the budget for the hard-to-hash set) against the oracle.
+  the budget for the hard-to-hash set), with fixed budgets of 1024 and 2048
+  keys, and with one selection per query head, each against the oracle.
 * stack32_b8_64k, one layer (batch 8, 65536 keys, top-1311): the same for the
   build, plus Algorithm 2 on sampled keys (each key hashes independently).
 * million_1m (1 048 576 keys, 128-bit codes, top-10486): the oracle cannot
@@ -97,13 +98,13 @@ def all_heads_property(sc, idx, k):
             check_selection_property(scn[b, h], idn[b, h], k, f"head {(b, h)}")
 
 
-def compare_sampled_head(d, P_ref, codes_ref, b, h, cfg, out, idx, sc, qc, label):
+def compare_sampled_head(d, P_ref, codes_ref, b, h, cfg, out, idx, sc, qc, label, k=None):
     Gq = cfg.G
     sm = 1.0 / np.sqrt(cfg.D)
     qb = bits(d["q"][b, h * Gq:(h + 1) * Gq])
     Kb = bits(d["K"][b, h, :cfg.N])
     Vb = bits(d["V"][b, h, :cfg.N])
-    ref = oracle.decode_head(qb, Kb, Vb, codes_ref, P_ref, cfg.k, sm)
+    ref = oracle.decode_head(qb, Kb, Vb, codes_ref, P_ref, cfg.k if k is None else k, sm)
     assert np.array_equal(u32(qc[b, h]), ref["qcode"]), f"{label}: query planes differ"
     assert np.array_equal(sc[b, h].cpu().numpy(), ref["scores"]), f"{label}: scores differ"
     assert np.array_equal(idx[b, h].cpu().numpy(), ref["idx"]), f"{label}: indices differ"
@@ -112,7 +113,7 @@ def compare_sampled_head(d, P_ref, codes_ref, b, h, cfg, out, idx, sc, qc, label
     assert np.all(e <= TOL), f"{label}: output error {e.max():.3g}"
 
 
-def build_decode_case(name, sample, hash_rows, eas=False):
+def build_decode_case(name, sample, hash_rows, eas=False, budgets=(), per_head=False):
     cfg = config_by_name(name)
     announce(f"[full size] {cfg}")
     d = make_layer(cfg, device=DEV)
@@ -151,6 +152,31 @@ def build_decode_case(name, sample, hash_rows, eas=False):
         announce(f"{name} head {(b, h)} with the safeguard ({int(ref['added'].sum())} of {m} added): "
                  f"max relative output error {e.max():.3g}")
         assert np.all(e <= TOL)
+    for kb in budgets:
+        # a fixed-count budget instead of the 2 % fraction, same launch path
+        out_b, idx_b, sc_b, qc_b = decode_full(d["q"], d["K"], d["V"], codes, P, kb, cfg.N)
+        all_heads_property(sc_b, idx_b, kb)
+        compare_sampled_head(d, P_ref, codes_ref, b, h, cfg, out_b, idx_b, sc_b, qc_b,
+                             f"{name} head {(b, h)} fixed budget k={kb}", k=kb)
+    if per_head:
+        # one selection per query head over the whole batch
+        idx_p = torch.empty(cfg.B, cfg.Hq, cfg.k, dtype=torch.int32, device=DEV)
+        sc_p = torch.empty(cfg.B, cfg.Hq, cfg.N, dtype=torch.int32, device=DEV)
+        out_p = bpc.decode_attention_per_head(d["q"], d["K"], d["V"], codes, P, cfg.k, N=cfg.N, idx_out=idx_p,
+                                              score_out=sc_p)
+        torch.cuda.synchronize()
+        scn, idn = sc_p.cpu().numpy(), idx_p.cpu().numpy()
+        for bb in range(cfg.B):
+            for j in range(cfg.Hq):
+                check_selection_property(scn[bb, j], idn[bb, j], cfg.k, f"per head {(bb, j)}")
+        rows = slice(h * cfg.G, (h + 1) * cfg.G)
+        ref = oracle.decode_per_query_head(bits(d["q"][b, rows]), Kb, bits(d["V"][b, h, :cfg.N]), codes_ref, P_ref,
+                                           cfg.k, 1.0 / np.sqrt(cfg.D))
+        assert np.array_equal(scn[b, rows], ref["scores"]), f"{name}: per-head scores differ"
+        assert np.array_equal(idn[b, rows], ref["idx"]), f"{name}: per-head indices differ"
+        e = rel_err(out_p[b, rows].cpu().numpy(), ref["out"])
+        announce(f"{name} head {(b, h)} per query head: max relative output error {e.max():.3g}")
+        assert np.all(e <= TOL)
     if hash_rows:
         rng = np.random.default_rng(cfg.seed)
         rows = np.unique(np.concatenate([rng.choice(cfg.N, hash_rows, replace=False), [0, cfg.N - 1]]))
@@ -163,7 +189,7 @@ def build_decode_case(name, sample, hash_rows, eas=False):
 
 @pytest.mark.timeout(600)
 def test_fullsize_batch16_128k():
-    build_decode_case("batch16_128k", sample=(11, 6), hash_rows=0, eas=True)
+    build_decode_case("batch16_128k", sample=(11, 6), hash_rows=0, eas=True, budgets=(1024, 2048), per_head=True)
 
 
 @pytest.mark.timeout(600)
