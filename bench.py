@@ -44,6 +44,9 @@ def parse():
     ap.add_argument("--instances", type=int, default=4)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-prefill", action="store_true")
+    ap.add_argument("--decode-only", action="store_true",
+                    help="skip the context measurements after the timed region (safeguard, fixed budgets, per "
+                         "query head, dense, offline calibration), so that a profile holds only the decode step")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run a plain 1 GiB device copy (counter calibration for rocprofv3 --pmc)")
     ap.add_argument("--cpu-sample-heads", type=int, default=128)
@@ -266,135 +269,137 @@ def main():
     stages = {n: round(float(t) * 1e3, 2) for n, t in zip(bpc.DECODE_STAGE_NAMES, stage_ms)}  # microseconds
     log(f"stages (us): {stages}")
 
-    # ---------------------------------------------------------------- the error-aware safeguard (context)
-    # the same step with 10 % of the 2 % budget reserved for the hard-to-hash
-    # set: k_hash = 2359 by hash score, union with the 263 keys of largest
-    # reconstruction error chosen once at prefill
-    k_hash = k - (k + 9) // 10
-    m_eas = k - k_hash
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
-    ev[0].record()
-    for it in insts:
-        it["serr"] = bpc.select_hard(it["err"], m_eas)
-    ev[1].record()
-    torch.cuda.synchronize()
-    select_ms = ev[0].elapsed_time(ev[1]) / len(insts)
-    for j in range(args.warmup):
-        it = insts[j % len(insts)]
-        bpc.decode_attention(it["q"], it["K"], it["V"], it["codes"], it["P"], k_hash, sm, out=outs[j % len(insts)],
-                             serr=it["serr"], workspace=ws)
-    eas_steps = max(10, min(args.steps, 100))
-    ev[0].record()
-    for j in range(eas_steps):
-        it = insts[j % len(insts)]
-        bpc.decode_attention(it["q"], it["K"], it["V"], it["codes"], it["P"], k_hash, sm, out=outs[j % len(insts)],
-                             serr=it["serr"], workspace=ws)
-    ev[1].record()
-    torch.cuda.synchronize()
-    eas = {"us_per_step": round(ev[0].elapsed_time(ev[1]) / eas_steps * 1e3, 2), "k_hash": k_hash, "m": m_eas,
-           "select_hard_ms": round(select_ms, 3),
-           "what": "decode step over S_hash (top-2359 by hash score) united with S_err (263 keys of largest "
-                   "reconstruction error, chosen per (b, h) at prefill by select_hard)"}
-    log(f"safeguard: {eas}")
-
-    # ---------------------------------------------------------------- fixed-count budgets (context)
-    # the same step with k = 1024 and k = 2048 keys instead of 2 % of N
-    def timed(fn, nsteps):
+    eas, fixed, per_head, dense, opc = {}, {}, {}, {}, {}
+    if not args.decode_only:
+        # ---------------------------------------------------------------- the error-aware safeguard (context)
+        # the same step with 10 % of the 2 % budget reserved for the hard-to-hash
+        # set: k_hash = 2359 by hash score, union with the 263 keys of largest
+        # reconstruction error chosen once at prefill
+        k_hash = k - (k + 9) // 10
+        m_eas = k - k_hash
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        ev[0].record()
+        for it in insts:
+            it["serr"] = bpc.select_hard(it["err"], m_eas)
+        ev[1].record()
+        torch.cuda.synchronize()
+        select_ms = ev[0].elapsed_time(ev[1]) / len(insts)
         for j in range(args.warmup):
-            fn(j)
-        ev[0].record()
-        for j in range(nsteps):
-            fn(j)
-        ev[1].record()
-        torch.cuda.synchronize()
-        return ev[0].elapsed_time(ev[1]) / nsteps * 1e3
-
-    fixed = {}
-    for kb in (1024, 2048):
-        ws_b = torch.empty(bpc.decode_workspace_bytes(B, Hq, Hkv, N, L, kb), dtype=torch.uint8, device=dev)
-
-        def fixed_step(j, kb=kb, ws_b=ws_b):
             it = insts[j % len(insts)]
-            bpc.decode_attention(it["q"], it["K"], it["V"], it["codes"], it["P"], kb, sm, out=outs[j % len(insts)],
-                                 workspace=ws_b)
-
-        fixed[f"k{kb}_us_per_step"] = round(timed(fixed_step, max(10, min(args.steps, 100))), 2)
-        del ws_b
-    fixed["what"] = "the decode step with a fixed budget of 1024 or 2048 keys per (b, h)"
-    log(f"fixed budgets: {fixed}")
-
-    # ---------------------------------------------------------------- per-query-head selection (context)
-    ws_ph = torch.empty(bpc.decode_per_head_workspace_bytes(B, Hq, Hkv, N, L, k), dtype=torch.uint8, device=dev)
-
-    def per_head_step(j):
-        it = insts[j % len(insts)]
-        bpc.decode_attention_per_head(it["q"], it["K"], it["V"], it["codes"], it["P"], k, sm,
-                                      out=outs[j % len(insts)], workspace=ws_ph)
-
-    ph_us = timed(per_head_step, max(10, min(args.steps, 100)))
-    ph_bytes = B * Hq * N * W * 4 + B * Hq * k * 2 * D * 2 + B * Hq * L * D * 4 + B * Hq * D * (2 + 4)
-    per_head = {"us_per_step": round(ph_us, 2), "GBps": round(ph_bytes / (ph_us * 1e-6) / 1e9, 1),
-                "what": f"one selection of {k} keys per query head ({Hq // Hkv} scans of each KV head's codes and "
-                        f"{Hq // Hkv} gathers per (b, h))"}
-    del ws_ph
-    log(f"per query head: {per_head}")
-
-    # ---------------------------------------------------------------- dense decode attention (context)
-    # full attention over all 131072 keys of every (b, h): what the sparse
-    # step replaces (the paper quotes its speed-ups against dense attention)
-    ws_dense = torch.empty(int(bpc._lib.bpc_dense_workspace_bytes(B, Hq, Hkv, N, D)), dtype=torch.uint8, device=dev)
-    for j in range(3):
-        it = insts[j % len(insts)]
-        bpc.dense_attention(it["q"], it["K"], it["V"], sm, out=outs[j % len(insts)], workspace=ws_dense)
-    dense_steps = 10
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for j in range(dense_steps):
-        it = insts[j % len(insts)]
-        bpc.dense_attention(it["q"], it["K"], it["V"], sm, out=outs[j % len(insts)], workspace=ws_dense)
-    e1.record()
-    torch.cuda.synchronize()
-    dense_us = e0.elapsed_time(e1) / dense_steps * 1e3
-    dense_bytes = B * Hkv * N * 2 * D * 2 + B * Hq * D * (2 + 4)
-    dense = {"us_per_step": round(dense_us, 1), "GBps": round(dense_bytes / (dense_us * 1e-6) / 1e9, 1),
-             "sparse_speedup": round(dense_us / (ms_per_step * 1e3), 2),
-             "what": "dense decode attention over all keys (every K and V row read), the comparison point"}
-    del ws_dense
-    log(f"dense: {dense}")
-
-    # ---------------------------------------------------------------- offline projection calibration (context)
-    # one P per KV head built offline (Algorithm 1 over held-out keys), then
-    # the batch's prefill is Algorithm 2 against it and decode reads it with
-    # a zero batch stride
-    opc = {}
-    if not args.no_prefill:
-        Kcal = make_calibration_keys(cfg, layer=0, n_seq=1, device=dev)
-        ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+            bpc.decode_attention(it["q"], it["K"], it["V"], it["codes"], it["P"], k_hash, sm, out=outs[j % len(insts)],
+                                 serr=it["serr"], workspace=ws)
+        eas_steps = max(10, min(args.steps, 100))
         ev[0].record()
-        Pcal = bpc.build_hash(Kcal, insts[0]["G"])[0][0]
+        for j in range(eas_steps):
+            it = insts[j % len(insts)]
+            bpc.decode_attention(it["q"], it["K"], it["V"], it["codes"], it["P"], k_hash, sm, out=outs[j % len(insts)],
+                                 serr=it["serr"], workspace=ws)
         ev[1].record()
-        codes_opc, _ = bpc.hash_keys(insts[0]["K"], Pcal)
-        ev[2].record()
         torch.cuda.synchronize()
-        del Kcal
-        it = insts[0]
-        for j in range(5):
-            bpc.decode_attention(it["q"], it["K"], it["V"], codes_opc, Pcal, k, sm, out=outs[0], workspace=ws)
-        nrep = 50
+        eas = {"us_per_step": round(ev[0].elapsed_time(ev[1]) / eas_steps * 1e3, 2), "k_hash": k_hash, "m": m_eas,
+               "select_hard_ms": round(select_ms, 3),
+               "what": "decode step over S_hash (top-2359 by hash score) united with S_err (263 keys of largest "
+                       "reconstruction error, chosen per (b, h) at prefill by select_hard)"}
+        log(f"safeguard: {eas}")
+
+        # ---------------------------------------------------------------- fixed-count budgets (context)
+        # the same step with k = 1024 and k = 2048 keys instead of 2 % of N
+        def timed(fn, nsteps):
+            for j in range(args.warmup):
+                fn(j)
+            ev[0].record()
+            for j in range(nsteps):
+                fn(j)
+            ev[1].record()
+            torch.cuda.synchronize()
+            return ev[0].elapsed_time(ev[1]) / nsteps * 1e3
+
+        fixed = {}
+        for kb in (1024, 2048):
+            ws_b = torch.empty(bpc.decode_workspace_bytes(B, Hq, Hkv, N, L, kb), dtype=torch.uint8, device=dev)
+
+            def fixed_step(j, kb=kb, ws_b=ws_b):
+                it = insts[j % len(insts)]
+                bpc.decode_attention(it["q"], it["K"], it["V"], it["codes"], it["P"], kb, sm, out=outs[j % len(insts)],
+                                     workspace=ws_b)
+
+            fixed[f"k{kb}_us_per_step"] = round(timed(fixed_step, max(10, min(args.steps, 100))), 2)
+            del ws_b
+        fixed["what"] = "the decode step with a fixed budget of 1024 or 2048 keys per (b, h)"
+        log(f"fixed budgets: {fixed}")
+
+        # ---------------------------------------------------------------- per-query-head selection (context)
+        ws_ph = torch.empty(bpc.decode_per_head_workspace_bytes(B, Hq, Hkv, N, L, k), dtype=torch.uint8, device=dev)
+
+        def per_head_step(j):
+            it = insts[j % len(insts)]
+            bpc.decode_attention_per_head(it["q"], it["K"], it["V"], it["codes"], it["P"], k, sm,
+                                          out=outs[j % len(insts)], workspace=ws_ph)
+
+        ph_us = timed(per_head_step, max(10, min(args.steps, 100)))
+        ph_bytes = B * Hq * N * W * 4 + B * Hq * k * 2 * D * 2 + B * Hq * L * D * 4 + B * Hq * D * (2 + 4)
+        per_head = {"us_per_step": round(ph_us, 2), "GBps": round(ph_bytes / (ph_us * 1e-6) / 1e9, 1),
+                    "what": f"one selection of {k} keys per query head ({Hq // Hkv} scans of each KV head's codes and "
+                            f"{Hq // Hkv} gathers per (b, h))"}
+        del ws_ph
+        log(f"per query head: {per_head}")
+
+        # ---------------------------------------------------------------- dense decode attention (context)
+        # full attention over all 131072 keys of every (b, h): what the sparse
+        # step replaces (the paper quotes its speed-ups against dense attention)
+        ws_dense = torch.empty(int(bpc._lib.bpc_dense_workspace_bytes(B, Hq, Hkv, N, D)), dtype=torch.uint8, device=dev)
+        for j in range(3):
+            it = insts[j % len(insts)]
+            bpc.dense_attention(it["q"], it["K"], it["V"], sm, out=outs[j % len(insts)], workspace=ws_dense)
+        dense_steps = 10
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
-        for j in range(nrep):
-            bpc.decode_attention(it["q"], it["K"], it["V"], codes_opc, Pcal, k, sm, out=outs[0], workspace=ws)
+        for j in range(dense_steps):
+            it = insts[j % len(insts)]
+            bpc.dense_attention(it["q"], it["K"], it["V"], sm, out=outs[j % len(insts)], workspace=ws_dense)
         e1.record()
         torch.cuda.synchronize()
-        opc = {"calibration_build_ms": round(ev[0].elapsed_time(ev[1]), 3),
-               "prefill_hash_ms": round(ev[1].elapsed_time(ev[2]), 3),
-               "decode_us_per_step_same_instance": round(e0.elapsed_time(e1) / nrep * 1e3, 2),
-               "what": "P per KV head from Algorithm 1 over 131072 held-out keys; prefill = Algorithm 2 of the "
-                       "whole batch against it; decode with the shared P, one instance repeated (its data "
-                       "partly stays in the 256 MB last-level cache)"}
-        del codes_opc
-        log(f"offline calibration: {opc}")
+        dense_us = e0.elapsed_time(e1) / dense_steps * 1e3
+        dense_bytes = B * Hkv * N * 2 * D * 2 + B * Hq * D * (2 + 4)
+        dense = {"us_per_step": round(dense_us, 1), "GBps": round(dense_bytes / (dense_us * 1e-6) / 1e9, 1),
+                 "sparse_speedup": round(dense_us / (ms_per_step * 1e3), 2),
+                 "what": "dense decode attention over all keys (every K and V row read), the comparison point"}
+        del ws_dense
+        log(f"dense: {dense}")
+
+        # ---------------------------------------------------------------- offline projection calibration (context)
+        # one P per KV head built offline (Algorithm 1 over held-out keys), then
+        # the batch's prefill is Algorithm 2 against it and decode reads it with
+        # a zero batch stride
+        opc = {}
+        if not args.no_prefill:
+            Kcal = make_calibration_keys(cfg, layer=0, n_seq=1, device=dev)
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+            ev[0].record()
+            Pcal = bpc.build_hash(Kcal, insts[0]["G"])[0][0]
+            ev[1].record()
+            codes_opc, _ = bpc.hash_keys(insts[0]["K"], Pcal)
+            ev[2].record()
+            torch.cuda.synchronize()
+            del Kcal
+            it = insts[0]
+            for j in range(5):
+                bpc.decode_attention(it["q"], it["K"], it["V"], codes_opc, Pcal, k, sm, out=outs[0], workspace=ws)
+            nrep = 50
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for j in range(nrep):
+                bpc.decode_attention(it["q"], it["K"], it["V"], codes_opc, Pcal, k, sm, out=outs[0], workspace=ws)
+            e1.record()
+            torch.cuda.synchronize()
+            opc = {"calibration_build_ms": round(ev[0].elapsed_time(ev[1]), 3),
+                   "prefill_hash_ms": round(ev[1].elapsed_time(ev[2]), 3),
+                   "decode_us_per_step_same_instance": round(e0.elapsed_time(e1) / nrep * 1e3, 2),
+                   "what": "P per KV head from Algorithm 1 over 131072 held-out keys; prefill = Algorithm 2 of the "
+                           "whole batch against it; decode with the shared P, one instance repeated (its data "
+                           "partly stays in the 256 MB last-level cache)"}
+            del codes_opc
+            log(f"offline calibration: {opc}")
 
     # algorithmic bytes (per step): codes read, gathered K+V rows, P, q and out
     BH = B * Hkv
