@@ -677,6 +677,12 @@ struct AttendShared {
   uint32_t sel[kSlice / 32];  // the safeguard: bitmap of the slice's keys the hash selection took
 };
 
+// An empty instruction that reads and rewrites x: loads feeding it are all
+// waited for here, together.
+__device__ __forceinline__ void pin_regs(uint4& x) {
+  __asm__ volatile("" : "+v"(x.x), "+v"(x.y), "+v"(x.z), "+v"(x.w));
+}
+
 // One pass of a wavefront over nrows (1..kAttnRows) rows; lane l < nrows
 // holds the key index of row l in myidx.  Updates the wavefront's running
 // maximum Mx and sum Ls (uniform over the wavefront) and this lane's
@@ -860,13 +866,21 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(G 
     constexpr int RV = (kWinSlices * kWinRec / 4 + kAttnThreads - 1) / kAttnThreads;
     const int nv = nslices * (kWinRec / 4);
     const uint4* wsrc = reinterpret_cast<const uint4*>(win + (size_t)bh * nslices * kWinRec);
+    // every load of the round is unconditional (indices clamped), so that all
+    // of them are in flight before the first wait
     uint4 wv[RV];
 #pragma unroll
-    for (int r = 0; r < RV; ++r)
-      if (r * kAttnThreads < nv) wv[r] = wsrc[min((int)threadIdx.x + r * kAttnThreads, nv - 1)];
+    for (int r = 0; r < RV; ++r) wv[r] = wsrc[min((int)threadIdx.x + r * kAttnThreads, nv - 1)];
     const uint4 mym = *reinterpret_cast<const uint4*>(mtb + s * 4);
     load_cand(0);
-    load_queries();
+    uint4 qv = reinterpret_cast<const uint4*>(q + ((size_t)b * Hkv * G + (size_t)h * G) * kHeadDim)[min(
+        (int)threadIdx.x, G * kHeadDim / 8 - 1)];
+    // the values are taken here, so the compiler cannot sink each load into
+    // the conditional store that uses it (which would wait on them one by one)
+#pragma unroll
+    for (int r = 0; r < RV; ++r) pin_regs(wv[r]);
+    pin_regs(qv);
+    if (threadIdx.x < G * kHeadDim / 8) sh.q[threadIdx.x / (kHeadDim / 8)][threadIdx.x % (kHeadDim / 8)] = qv;
     uint4* wdst = reinterpret_cast<uint4*>(&sh.u.win[0][0]);
 #pragma unroll
     for (int r = 0; r < RV; ++r)
@@ -1277,7 +1291,7 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(G 
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kHeadDim) void merge_kernel(int Hkv, int G, int nchunks, const float* __restrict__ part,
                                                          float* __restrict__ out) {
-  constexpr int CB = 512;  // partials per pass
+  constexpr int MB = 8;  // partials per batch: all of a batch's loads are issued before the first is used
   const int bq = blockIdx.x;  // b * Hq + query head
   const int Hq = Hkv * G;
   const int b = bq / Hq, jq = bq % Hq;
@@ -1285,34 +1299,37 @@ __global__ __launch_bounds__(kHeadDim) void merge_kernel(int Hkv, int G, int nch
   const size_t bh = (size_t)b * Hkv + h;
   const size_t cstride = (size_t)G * (kHeadDim + 2);
   const float* pg = part + bh * nchunks * cstride + (size_t)g * (kHeadDim + 2);
+  const int d = threadIdx.x;
   BPC_STAMP(3, 0);
-  __shared__ float m_s[CB], l_s[CB];
-  __shared__ float mx_s[2];
-  // global maximum: the partial maxima are loaded in parallel
-  float mloc = -INFINITY;
-  for (int t = threadIdx.x; t < nchunks; t += kHeadDim) mloc = fmaxf(mloc, pg[t * cstride]);
+  // one pass with a running maximum: each thread reads every partial's
+  // (max, sum) and its own coordinate of the weighted V
+  float M = -INFINITY, lsum = 0.f, acc = 0.f;
+  for (int t0 = 0; t0 < nchunks; t0 += MB) {
+    float mt[MB], lt[MB], ot[MB];
 #pragma unroll
-  for (int o = 1; o < 64; o <<= 1) mloc = fmaxf(mloc, __shfl_xor(mloc, o, 64));
-  if ((threadIdx.x & 63) == 0) mx_s[threadIdx.x >> 6] = mloc;
-  __syncthreads();
-  const float Mx = fmaxf(mx_s[0], mx_s[1]);
-  float acc = 0.f, lsum = 0.f;
-  for (int t0 = 0; t0 < nchunks; t0 += CB) {
-    const int nc = min(CB, nchunks - t0);
-    for (int t = threadIdx.x; t < nc; t += kHeadDim) {
-      const float mt = pg[(t0 + t) * cstride];
-      m_s[t] = (mt == -INFINITY) ? 0.f : exp2f(mt - Mx);
-      l_s[t] = pg[(t0 + t) * cstride + 1];
+    for (int u = 0; u < MB; ++u) {
+      const float* pc = pg + (size_t)min(t0 + u, nchunks - 1) * cstride;
+      mt[u] = pc[0], lt[u] = pc[1], ot[u] = pc[2 + d];
     }
-    __syncthreads();
-#pragma unroll 8
-    for (int t = 0; t < nc; ++t) {
-      lsum = fmaf(l_s[t], m_s[t], lsum);
-      acc = fmaf(pg[(t0 + t) * cstride + 2 + threadIdx.x], m_s[t], acc);
+    float mb = -INFINITY;
+#pragma unroll
+    for (int u = 0; u < MB; ++u) {
+      if (t0 + u >= nchunks) mt[u] = -INFINITY;  // past the last partial: dropped
+      mb = fmaxf(mb, mt[u]);
     }
-    __syncthreads();
+    const float Mn = fmaxf(M, mb);
+    if (Mn == -INFINITY) continue;  // no partial with a key so far
+    const float f = (M == -INFINITY) ? 0.f : exp2f(M - Mn);
+    lsum *= f, acc *= f;
+#pragma unroll
+    for (int u = 0; u < MB; ++u) {
+      const float w = (mt[u] == -INFINITY) ? 0.f : exp2f(mt[u] - Mn);
+      lsum = fmaf(lt[u], w, lsum);
+      acc = fmaf(ot[u], w, acc);
+    }
+    M = Mn;
   }
-  out[(size_t)bq * kHeadDim + threadIdx.x] = acc / lsum;
+  out[(size_t)bq * kHeadDim + d] = acc / lsum;
   BPC_STAMP(3, 1);
 }
 
