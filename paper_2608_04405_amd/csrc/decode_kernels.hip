@@ -610,32 +610,24 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(L
 //     their distance is below T* or at T* within the quota; the kept keys
 //     (ascending) go to the LDS row list and to idx_out.
 //  c. Attention: each wavefront runs independently over rows of the list,
-//     16 per pass: sixteen lanes share a key row (lane l16 holds dims
-//     [8 l16, 8 l16 + 8)), every K and V load of a pass is issued before the
-//     first is consumed, logits use bf16 dot2 and DPP row sums and stay in
-//     base 2 (sm_scale * log2 e), and the wavefront carries its own running
-//     (max, sum, weighted V).  The four wavefronts are combined once, into
-//     one partial per query head.
+//     16 per pass; every K and V load of a pass is issued before the first
+//     is consumed.  The logits of the pass's 16 rows and the group's query
+//     heads are one 16 x 16 x 128 product on the matrix cores (rows x heads,
+//     heads padded to 16), in base 2 (sm_scale * log2 e); they reach the
+//     lanes holding the V rows through LDS.  Sixteen lanes share a V row
+//     (lane l16 holds dims [8 l16, 8 l16 + 8)), and the wavefront carries
+//     its own running (max, sum, weighted V).  The four wavefronts are
+//     combined once, into one partial per query head.
 // ---------------------------------------------------------------------------
-typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef short bf16x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
-// a + (bf16 pair x) . (bf16 pair y), fp32 accumulation
-__device__ __forceinline__ float dot2_bf16(uint32_t x, uint32_t y, float a) {
-  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, x), __builtin_bit_cast(bf16x2_t, y), a, false);
-}
-
-// sum over each row of 16 lanes, every lane of the row receives it (DPP:
-// swap neighbours, swap pairs, mirror within 8, mirror within 16)
-template <int CTRL>
-__device__ __forceinline__ float dpp_f32(float v) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), CTRL, 0xF, 0xF, true));
-}
-__device__ __forceinline__ float row16_sum(float v) {
-  v += dpp_f32<0xB1>(v);
-  v += dpp_f32<0x4E>(v);
-  v += dpp_f32<0x141>(v);
-  v += dpp_f32<0x140>(v);
-  return v;
+// D += A B for one 16 x 16 x 16 bf16 tile (fp32 accumulation).  Lane i
+// supplies A[i % 16][4 (i / 16) + j] and B[4 (i / 16) + j][i % 16] (j = 0..3,
+// two bf16 per 32-bit word, low half first) and holds D[4 (i / 16) + j][i % 16].
+__device__ __forceinline__ f32x4_t mfma16(uint32_t a0, uint32_t a1, uint32_t b0, uint32_t b1, f32x4_t d) {
+  return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(bf16x4_t, make_uint2(a0, a1)),
+                                                   __builtin_bit_cast(bf16x4_t, make_uint2(b0, b1)), d, 0, 0, 0);
 }
 
 __device__ __forceinline__ void unpack8(const uint4 v, float (&f)[8]) {
@@ -646,8 +638,7 @@ __device__ __forceinline__ void unpack8(const uint4 v, float (&f)[8]) {
 }
 
 constexpr int kAttnWaves = kAttnThreads / 64;
-constexpr int kAttnSlots = 4;                // rows per lane per pass
-constexpr int kAttnRows = 4 * kAttnSlots;    // rows per wavefront per pass
+constexpr int kAttnRows = 16;                // rows per wavefront per pass (one 16-row tile)
 constexpr int kPlanCache = 16;               // slices whose histograms are kept in LDS
 constexpr int kRoundBatch = 8;               // histogram loads per thread issued together
 constexpr int kRowCache = 2048;              // selected rows kept in LDS (more go through global memory)
@@ -669,6 +660,7 @@ struct AttendShared {
     float o[kAttnWaves][G][kHeadDim];   // per-wavefront weighted V
   } u;
   float st[kAttnWaves][G][2];  // per wavefront (max, sum)
+  alignas(16) float pl[kAttnWaves][G][16];  // per wavefront: the logits of a pass, handed between lanes
   uint4 q[G][kHeadDim / 8];     // the group's queries, bf16
   int wave_tot[kAttnWaves];
   int first[2];
@@ -684,68 +676,90 @@ __device__ __forceinline__ void pin_regs(uint4& x) {
 }
 
 // One pass of a wavefront over nrows (1..kAttnRows) rows; lane l < nrows
-// holds the key index of row l in myidx.  Updates the wavefront's running
-// maximum Mx and sum Ls (uniform over the wavefront) and this lane's
-// weighted-V partials o.
+// holds the key index of row l in myidx; pl is the wavefront's [G][16] LDS
+// area for the logits.  Updates the wavefront's running maximum Mx and sum
+// Ls (uniform over the wavefront) and this lane's weighted-V partials o.
+//
+// Logits: lane (r, c) = (lane / 16, lane % 16) loads dims [32 kb + 8 r, +8)
+// of K row c (kb = 0..3) and, as the second operand, the same dims of query
+// head c (zero for c >= G); each 16-byte load feeds two tiles (dims +0..3
+// and +4..7), so eight tiles cover the 128 dims.  The result, D[row][head],
+// lands in lane (r, head) for rows 4 r .. 4 r + 3.  V: lane (r, c) loads
+// dims [8 c, 8 c + 8) of rows 4 r .. 4 r + 3, which are exactly the rows
+// whose logits the lanes (r, head < G) of its own group hold.
 template <int G>
-__device__ __forceinline__ void attend_pass(int myidx, int nrows, const uint4 (*qs)[kHeadDim / 8], const char* Kh,
-                                            uint32_t kstride, const char* Vh, uint32_t vstride, float scale_log2,
-                                            float (&Mx)[G], float (&Ls)[G], float (&o)[G][8]) {
+__device__ __forceinline__ void attend_pass(int myidx, int nrows, const uint4 (*qs)[kHeadDim / 8], float (*pl)[16],
+                                            const char* Kh, uint32_t kstride, const char* Vh, uint32_t vstride,
+                                            float scale_log2, float (&Mx)[G], float (&Ls)[G], float (&o)[G][8]) {
+  static_assert(G <= 16, "the query heads of a group fill at most the 16 columns of a tile");
   const int lane = threadIdx.x & 63;
-  const int l16 = lane & 15, rsub = lane >> 4;
-  bool ok[kAttnSlots];
-  uint32_t rown[kAttnSlots];
+  const int c16 = lane & 15, r4 = lane >> 4;
+  const uint32_t nk = (uint32_t)__shfl(myidx, c16, 64);
+  const uint32_t rk = c16 < nrows ? nk : 0u;  // row 0 of the head always exists
+  uint32_t rv[4];
 #pragma unroll
-  for (int it = 0; it < kAttnSlots; ++it) {
-    const uint32_t n = (uint32_t)__shfl(myidx, it * 4 + rsub, 64);
-    ok[it] = it * 4 + rsub < nrows;
-    rown[it] = ok[it] ? n : 0u;  // row 0 of the head always exists
+  for (int t = 0; t < 4; ++t) {
+    const uint32_t n = (uint32_t)__shfl(myidx, 4 * r4 + t, 64);
+    rv[t] = 4 * r4 + t < nrows ? n : 0u;
   }
-  uint4 kv[kAttnSlots], vv[kAttnSlots];
+  uint4 kv[4], vv[4];
 #pragma unroll
-  for (int it = 0; it < kAttnSlots; ++it)
-    kv[it] = *reinterpret_cast<const uint4*>(Kh + (rown[it] * kstride + 16u * l16));
+  for (int kb = 0; kb < 4; ++kb) kv[kb] = *reinterpret_cast<const uint4*>(Kh + (rk * kstride + 64u * kb + 16u * r4));
 #pragma unroll
-  for (int it = 0; it < kAttnSlots; ++it)
-    vv[it] = *reinterpret_cast<const uint4*>(Vh + (rown[it] * vstride + 16u * l16));
-  // logits of the lane's rows (it * 4 + rsub): bf16 dot2 (exact products,
-  // fp32 sums), then a DPP sum over the 16 lanes of the row
-  float lg[G][kAttnSlots];
-  int qi = l16;
+  for (int t = 0; t < 4; ++t) vv[t] = *reinterpret_cast<const uint4*>(Vh + (rv[t] * vstride + 16u * c16));
+  // logits on the matrix cores
+  int qi = c16;
   __asm__ volatile("" : "+v"(qi));  // the query is re-read from LDS each pass, not held in registers
+  f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-  for (int g = 0; g < G; ++g) {
-    const uint4 qg = qs[g][qi];  // eight bf16 of query head g, as four packed pairs
-#pragma unroll
-    for (int it = 0; it < kAttnSlots; ++it) {
-      float a = dot2_bf16(kv[it].x, qg.x, 0.f);
-      a = dot2_bf16(kv[it].y, qg.y, a);
-      a = dot2_bf16(kv[it].z, qg.z, a);
-      a = dot2_bf16(kv[it].w, qg.w, a);
-      a = row16_sum(a);  // outside the condition: every lane takes part in the DPP sum
-      lg[g][it] = ok[it] ? a * scale_log2 : -INFINITY;
-    }
+  for (int kb = 0; kb < 4; ++kb) {
+    const uint4 qv = qi < G ? qs[qi][4 * kb + r4] : make_uint4(0u, 0u, 0u, 0u);
+    acc = mfma16(kv[kb].x, kv[kb].y, qv.x, qv.y, acc);
+    acc = mfma16(kv[kb].z, kv[kb].w, qv.z, qv.w, acc);
   }
-  // running maximum and sum (uniform over the wavefront: kept in scalar
-  // registers); lg becomes the weights p
+  if (c16 < G) {
+    float4 w;
+    w.x = 4 * r4 + 0 < nrows ? acc[0] * scale_log2 : -INFINITY;
+    w.y = 4 * r4 + 1 < nrows ? acc[1] * scale_log2 : -INFINITY;
+    w.z = 4 * r4 + 2 < nrows ? acc[2] * scale_log2 : -INFINITY;
+    w.w = 4 * r4 + 3 < nrows ? acc[3] * scale_log2 : -INFINITY;
+    *reinterpret_cast<float4*>(&pl[c16][4 * r4]) = w;
+  }
+  // LDS operations of one wavefront complete in order: the reads below see
+  // the writes above; this only keeps the compiler from moving them across
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  float lg[G][4];
 #pragma unroll
   for (int g = 0; g < G; ++g) {
-    float m = -INFINITY;
+    const float4 x = *reinterpret_cast<const float4*>(&pl[g][4 * r4]);
+    lg[g][0] = x.x, lg[g][1] = x.y, lg[g][2] = x.z, lg[g][3] = x.w;
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();  // the next pass rewrites pl only after these reads
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  // running maximum and sum, uniform over the wavefront: the lanes of a row
+  // group hold the same four rows, so lanes 0, 16, 32 and 48 carry the four
+  // groups' partial results
 #pragma unroll
-    for (int it = 0; it < kAttnSlots; ++it) m = fmaxf(m, lg[g][it]);
-    m = fmaxf(m, __shfl_xor(m, 16, 64));
-    m = fmaxf(m, __shfl_xor(m, 32, 64));
+  for (int g = 0; g < G; ++g) {
+    float m = fmaxf(fmaxf(lg[g][0], lg[g][1]), fmaxf(lg[g][2], lg[g][3]));
+    const int mb = __float_as_int(m);
+    m = fmaxf(fmaxf(__int_as_float(__builtin_amdgcn_readlane(mb, 0)), __int_as_float(__builtin_amdgcn_readlane(mb, 16))),
+              fmaxf(__int_as_float(__builtin_amdgcn_readlane(mb, 32)), __int_as_float(__builtin_amdgcn_readlane(mb, 48))));
     const float mnew = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(fmaxf(Mx[g], m))));
     // rescale what earlier passes accumulated (Mx = -inf before the first: factor 0)
     const float f = (Mx[g] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(Mx[g] - mnew);
     float ps = 0.f;
 #pragma unroll
-    for (int it = 0; it < kAttnSlots; ++it) {
-      lg[g][it] = ok[it] ? __builtin_amdgcn_exp2f(lg[g][it] - mnew) : 0.f;
-      ps += lg[g][it];
+    for (int t = 0; t < 4; ++t) {
+      lg[g][t] = __builtin_amdgcn_exp2f(lg[g][t] - mnew);  // a masked row: exp2(-inf) = 0
+      ps += lg[g][t];
     }
-    ps += __shfl_xor(ps, 16, 64);
-    ps += __shfl_xor(ps, 32, 64);
+    const int pb = __float_as_int(ps);
+    ps = (__int_as_float(__builtin_amdgcn_readlane(pb, 0)) + __int_as_float(__builtin_amdgcn_readlane(pb, 16))) +
+         (__int_as_float(__builtin_amdgcn_readlane(pb, 32)) + __int_as_float(__builtin_amdgcn_readlane(pb, 48)));
     Ls[g] = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(Ls[g] * f + ps)));
     Mx[g] = mnew;
 #pragma unroll
@@ -753,13 +767,13 @@ __device__ __forceinline__ void attend_pass(int myidx, int nrows, const uint4 (*
   }
   // weighted V of the lane's rows
 #pragma unroll
-  for (int it = 0; it < kAttnSlots; ++it) {
+  for (int t = 0; t < 4; ++t) {
     float vf[8];
-    unpack8(vv[it], vf);
+    unpack8(vv[t], vf);
 #pragma unroll
     for (int g = 0; g < G; ++g)
 #pragma unroll
-      for (int e = 0; e < 8; ++e) o[g][e] = fmaf(lg[g][it], vf[e], o[g][e]);
+      for (int e = 0; e < 8; ++e) o[g][e] = fmaf(lg[g][t], vf[e], o[g][e]);
   }
 }
 
@@ -1218,12 +1232,12 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(G 
   if (rows_lds) {
     for (int r0 = wid * kAttnRows; r0 < kept; r0 += kAttnWaves * kAttnRows) {
       const int nr = min(kAttnRows, kept - r0);
-      attend_pass<G>(lane < nr ? sh.u.rows[r0 + lane] : 0, nr, sh.q, Kh, kstride, Vh, vstride, scale_log2, Mx, Ls, o);
+      attend_pass<G>(lane < nr ? sh.u.rows[r0 + lane] : 0, nr, sh.q, sh.pl[wid], Kh, kstride, Vh, vstride, scale_log2, Mx, Ls, o);
     }
   } else {
     for (int r0 = wid * kAttnRows; r0 < kept; r0 += kAttnWaves * kAttnRows) {
       const int nr = min(kAttnRows, kept - r0);
-      attend_pass<G>(lane < nr ? grows[r0 + lane] : 0, nr, sh.q, Kh, kstride, Vh, vstride, scale_log2, Mx, Ls, o);
+      attend_pass<G>(lane < nr ? grows[r0 + lane] : 0, nr, sh.q, sh.pl[wid], Kh, kstride, Vh, vstride, scale_log2, Mx, Ls, o);
     }
   }
   BPC_STAMP(2, 5);
@@ -1247,6 +1261,7 @@ template <int G>
 struct DenseShared {
   float o[kAttnWaves][G][kHeadDim];
   float st[kAttnWaves][G][2];
+  alignas(16) float pl[kAttnWaves][G][16];
   uint4 q[G][kHeadDim / 8];
 };
 
@@ -1277,7 +1292,7 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(G 
   }
   for (int r0 = wid * kAttnRows; r0 < cnt; r0 += kAttnWaves * kAttnRows) {
     const int nr = min(kAttnRows, cnt - r0);
-    attend_pass<G>(lane < nr ? n0 + r0 + lane : 0, nr, sh.q, Kh, kstride, Vh, vstride, scale_log2, Mx, Ls, o);
+    attend_pass<G>(lane < nr ? n0 + r0 + lane : 0, nr, sh.q, sh.pl[wid], Kh, kstride, Vh, vstride, scale_log2, Mx, Ls, o);
   }
   write_partial<G>(sh.o, sh.st, Mx, Ls, o, part + (size_t)blockIdx.x * G * (kHeadDim + 2));
 }
