@@ -408,8 +408,8 @@ def main():
     p_bytes = BH * L * D * 4
     qo_bytes = B * Hq * D * (2 + 4)
     step_bytes = code_bytes + gather_bytes + p_bytes + qo_bytes
-    per_kernel_bytes = {"score": code_bytes, "attend": gather_bytes + B * Hq * D * 2,
-                        "qpack": p_bytes + B * Hq * D * 2}
+    # the scoring kernel also packs the query (P and q of every (b, h))
+    per_kernel_bytes = {"score": code_bytes + p_bytes + B * Hq * D * 2, "attend": gather_bytes + B * Hq * D * 2}
     # dominant kernel: the stage with the largest time among the HBM streamers
     dom = max(("score", "attend"), key=lambda n: stages[n])
     dom_us = stages[dom]

@@ -200,7 +200,7 @@ int bpc_append_kv(const uint16_t* k_new, int64_t sKn_b, int64_t sKn_h, int64_t s
  * workspace  at least bpc_decode_workspace_bytes(...) bytes, 256-byte
  *            aligned; contents on entry do not matter.  Two calls that use
  *            the same workspace must be ordered on one stream.
- * Cost: four kernel launches (query packing, scoring, threshold with
+ * Cost: three kernel launches (query packing with scoring, threshold with
  * selection and attention, merge of the per-slice partials), plus one for a
  * ragged last slice or codes whose strides are not multiples of 4 words.
  */
@@ -238,7 +238,7 @@ int bpc_decode_attention(const uint16_t* q,
  * Cost: the codes of a KV head are scanned once per query head (G times
  * the code traffic of bpc_decode_attention) and G selections are gathered.
  * When the batch stride of K, V, codes and P is Hkv times the head stride
- * (contiguous heads) the batch is one launch sequence of four kernels;
+ * (contiguous heads) the batch is one launch sequence of three kernels;
  * otherwise one per sequence.  Errors as for bpc_decode_attention.
  */
 size_t bpc_decode_per_head_workspace_bytes(int B, int Hq, int Hkv, int N, int D, int L, int k);
@@ -332,11 +332,11 @@ int bpc_dense_attention(const uint16_t* q,
 /*
  * bpc_decode_attention_profiled -- bpc_decode_attention that also records
  * caller-created hipEvent_t handles on `stream` at the stage boundaries
- * (query packing | scoring | threshold, selection and attention | merge):
+ * (query packing and scoring | threshold, selection and attention | merge):
  * events[0] before the first stage and events[s + 1] after stage s, so
  * n_events must be BPC_DECODE_STAGES + 1.  For measuring only.
  */
-#define BPC_DECODE_STAGES 4
+#define BPC_DECODE_STAGES 3
 int bpc_decode_attention_profiled(const uint16_t* q,
                                   const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t sK_n,
                                   const uint16_t* V, int64_t sV_b, int64_t sV_h, int64_t sV_n,

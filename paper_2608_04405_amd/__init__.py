@@ -83,8 +83,8 @@ _lib.bpc_select_hard.argtypes = [_p, _i64, _i64, _i, _i, _i, _i, _p, _p]
 _lib.bpc_decode_attention_profiled.restype = _i
 _lib.bpc_decode_attention_profiled.argtypes = _DECODE_ARGS + [ctypes.POINTER(_p), _i]
 
-DECODE_STAGES = 4
-DECODE_STAGE_NAMES = ("qpack", "score", "attend", "merge")
+DECODE_STAGES = 3
+DECODE_STAGE_NAMES = ("score", "attend", "merge")
 
 
 class BPCError(RuntimeError):

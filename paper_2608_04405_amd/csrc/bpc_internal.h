@@ -20,7 +20,6 @@ constexpr int kHeadDim = 128;
 // histogram in LDS.  At most kMaxSlices slices per (sequence, KV head).
 constexpr int kSlice = 16384;
 constexpr int kScoreThreads = 512;  // scoring workgroup: 32 keys per thread
-constexpr int kScanThreads = 1024;  // query-packing workgroup
 constexpr int kMaxSlices = 1024;
 // One attention workgroup per slice keeps its selected candidates, read in
 // batches of kCandBatch, and gathers their rows with four wavefronts.
@@ -189,6 +188,41 @@ __device__ __forceinline__ int block_exclusive_scan(int v, int* wave_tot, int& t
 }
 
 // lowest set lane of a 64-bit ballot, or 64
+// ---------------------------------------------------------------------------
+// block-wide exclusive scan of one non-negative int per thread whose set
+// bits all lie in MASK, without cross-lane shuffles: within a wavefront the
+// prefix is sum_b 2^b * (lanes below with bit b set), one ballot and one
+// mbcnt per bit of MASK; the wavefront totals go through LDS with one
+// barrier.  Two counts can be scanned at once as (c1 << 16) | c0 when every
+// sum of c0 stays below 2^16.  wave_tot[2][NW]: consecutive calls must
+// alternate `buf` (0, 1, 0, ...) so that a call never overwrites totals
+// another thread may still be reading.
+// ---------------------------------------------------------------------------
+template <int NT, uint32_t MASK>
+__device__ __forceinline__ int block_exclusive_scan_bits(int v, int (*wave_tot)[NT / 64], int buf, int& total) {
+  constexpr int NW = NT / 64;
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  int below = 0, wtot = 0;
+#pragma unroll
+  for (int b = 0; b < 32; ++b) {
+    if (!((MASK >> b) & 1u)) continue;
+    const unsigned long long m = __ballot((v >> b) & 1);
+    below += (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u)) << b;
+    wtot += (int)__popcll(m) << b;
+  }
+  if (lane == 0) wave_tot[buf][wid] = wtot;
+  __syncthreads();
+  int before = 0, tot = 0;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) {
+    const int t = wave_tot[buf][w];
+    before += (w < wid) ? t : 0;
+    tot += t;
+  }
+  total = tot;
+  return before + below;
+}
+
 __device__ __forceinline__ int first_lane(unsigned long long m) { return m ? __ffsll((long long)m) - 1 : 64; }
 
 }  // namespace bpc

@@ -12,8 +12,9 @@
 //             group (every slice of (b, h) does it; they share an XCD, so P
 //             comes from HBM once), scores the slice's codes into an LDS
 //             histogram, finds the slice's own k-th smallest distance kth_s,
-//             and writes its histograms up to kth_s and its candidates
-//             (dist <= kth_s) in key order.
+//             and writes its histograms up to kth_s, a window record of
+//             cumulative counts around its share of the threshold, and its
+//             candidates (dist <= cand_max <= kth_s) in key order.
 //   2 attend  one workgroup per slice: from the histograms of every slice of
 //             (b, h) it derives the global k-th smallest distance T*, how
 //             many keys at T* its slice keeps (lowest indices first) and its
@@ -50,6 +51,7 @@ __device__ unsigned long long* g_trace = nullptr;
   do {                                                                                        \
     BPC_NOTE(kern, slot, __builtin_amdgcn_s_memrealtime());                                   \
     if ((slot) == 0) BPC_NOTE(kern, 15, __builtin_amdgcn_s_getreg((3 << 11) | 20) & 15);      \
+    if ((slot) == 0) BPC_NOTE(kern, 11, __builtin_amdgcn_s_getreg((31 << 11) | 4));          \
   } while (0)
 #else
 #define BPC_STAMP(kern, slot) ((void)0)
@@ -70,166 +72,164 @@ __device__ __forceinline__ void slice_tile(int id, int BH, int nslices, int& bh,
 }
 
 // ---------------------------------------------------------------------------
-// Query projection, quantisation and packing by a 1024-thread workgroup.
-// P and q are staged in LDS; each fixed-order dot is split over a quad of
-// lanes (lane c sums coordinates [32c, 32c + 32) in ascending order) and the
-// quad combines its block sums as ((b0 + b1) + (b2 + b3)).  Results land in
-// LDS: qc[8 W] (plane 0 = signs, plane 1 + j = bit j of |p|) and *T =
-// sum |p_i|.  Ends with a barrier.
+// Query projection, quantisation and packing (Sec. 3.2 "Retrieval Phase";
+// Appendix "Packing kernel"), done by every scoring workgroup for its own
+// (b, h) before its first code load, so that the loads of P and q are not
+// queued behind the code stream of other workgroups.  All slices of a
+// (b, h) run on one XCD: P and q come from HBM once, then from its L2.
+//
+// P is loaded with coalesced 16-byte loads and staged in LDS (in the place
+// of the slice histogram), 16-byte unit r of block c = coordinates
+// [32 c + 4 r, 32 c + 4 r + 4) of row i at i 32 + 8 c + (r ^ (c + 4 (i & 1))):
+// the eight lanes (two rows x four blocks) that read one unit index at a
+// time then hit eight different bank groups.  Thread t < 4 L owns block
+// c = t mod 4 of row i = t / 4: for each query head g, in ascending order,
+// it sums its 32 coordinates in ascending order from +0, the quad of lanes
+// sharing i combines the block sums as ((b0 + b1) + (b2 + b3)), and the
+// heads are added in ascending g.  Each product of a bf16 query coordinate
+// and an fp32 entry of P is exact in fp64 (8 + 24 significant bits), so a
+// fused multiply-add rounds exactly as the separately rounded multiply and
+// add would.  The group sum is quantised to [-127, 127] (scale 127 / max |x|,
+// rounded half away from zero) and packed into 1 sign + 7 magnitude planes.
 // ---------------------------------------------------------------------------
 template <int L>
 struct QpackShared {
-  static constexpr int PADB = 33;  // 32 coordinates per block + 1 to skew LDS banks
-  float P_s[L][4][PADB];
-  float q_s[kMaxGroup][4][PADB];
-  double x_s[kMaxGroup][L];
-  double xbar_s[L];
-  double mx_s;
-  int tsum_s[2];
+  float4 P[L * 32];                  // P, 16-byte units in the swizzled order above
+  uint4 q[kMaxGroup][kHeadDim / 8];  // the group's queries, bf16
 };
 
-// The global loads of the query packing (P rows and the group's queries),
-// issued ahead of everything else by the caller.
-template <int L, int NT>
-struct QpackRegs {
-  static constexpr int PV = L * kHeadDim / 4 / NT;                  // float4 of P per thread
-  static constexpr int QV = (kMaxGroup * kHeadDim / 8 + NT - 1) / NT;  // uint4 of q per thread (at most)
-  float4 pv[PV];
-  uint4 qv[QV];
+// small per-workgroup state of the packing (kept outside the histogram)
+template <int L>
+struct QpackOut {
+  double wmax[kScoreThreads / 64];  // max |xbar| per wavefront
+  uint16_t qc16[8 * (L / 16)];      // the planes as 16-bit pieces (little-endian words of qc)
 };
 
-template <int L, int NT>
-__device__ __forceinline__ void qpack_load(QpackRegs<L, NT>& r, const uint16_t* __restrict__ q,
-                                           const float* __restrict__ P, int64_t sP_b, int64_t sP_h, int Hkv, int G,
-                                           int bh) {
-  static_assert(NT >= 128 && L * kHeadDim / 4 % NT == 0, "thread count");
-  const int b = bh / Hkv, h = bh % Hkv;
-  const float* Pb = P + b * sP_b + h * sP_h;
-  const uint16_t* qb = q + ((size_t)b * Hkv * G + (size_t)h * G) * kHeadDim;
-#pragma unroll
-  for (int i = 0; i < QpackRegs<L, NT>::PV; ++i) r.pv[i] = reinterpret_cast<const float4*>(Pb)[i * NT + threadIdx.x];
-#pragma unroll
-  for (int i = 0; i < QpackRegs<L, NT>::QV; ++i) {
-    const int e = i * NT + threadIdx.x;
-    r.qv[i] = (e < G * kHeadDim / 8) ? reinterpret_cast<const uint4*>(qb)[e] : make_uint4(0, 0, 0, 0);
-  }
+__device__ __forceinline__ int qpack_swz(int i, int c) { return c + 4 * (i & 1); }
+
+// x of lane l ^ 1 and of lane l ^ 2 (DPP quad permutations), for doubles
+template <int CTRL>
+__device__ __forceinline__ double dpp_f64(double x) {
+  const int lo = __builtin_amdgcn_mov_dpp(__double2loint(x), CTRL, 0xF, 0xF, false);
+  const int hi = __builtin_amdgcn_mov_dpp(__double2hiint(x), CTRL, 0xF, 0xF, false);
+  return __hiloint2double(hi, lo);
+}
+constexpr int kDppQuadXor1 = 0xB1;    // quad_perm [1, 0, 3, 2]
+constexpr int kDppQuadXor2 = 0x4E;    // quad_perm [2, 3, 0, 1]
+constexpr int kDppHalfMirror = 0x141;  // lane i <-> 7 - i within 8 lanes
+constexpr int kDppMirror = 0x140;      // lane i <-> 15 - i within 16 lanes
+
+// bit 4 k of m, for k = 0..15, packed into the low 16 bits
+__device__ __forceinline__ uint32_t every_fourth_bit(unsigned long long m) {
+  m &= 0x1111111111111111ull;
+  m = (m | (m >> 3)) & 0x0303030303030303ull;
+  m = (m | (m >> 6)) & 0x000F000F000F000Full;
+  m = (m | (m >> 12)) & 0x000000FF000000FFull;
+  m = (m | (m >> 24)) & 0x000000000000FFFFull;
+  return (uint32_t)m;
 }
 
+// The planes land in o.qc16 (read them as 8 W little-endian u32 words: plane
+// 0 = signs, plane 1 + j = bit j of |p|).  Ends with a barrier; sh is free
+// after it.
 template <int L, int NT>
-__device__ __forceinline__ void qpack_body(QpackShared<L>& sh, const QpackRegs<L, NT>& r, int G, uint32_t* qc,
-                                           int* T) {
-  constexpr int W = L / 32;
+__device__ __forceinline__ void qpack_block(QpackShared<L>& sh, QpackOut<L>& o, const uint16_t* __restrict__ qg,
+                                            const float* __restrict__ Pbh, int G) {
+  static_assert((L * 32) % NT == 0 && 4 * L <= NT, "thread count");
+  constexpr int PV = L * 32 / NT;  // 16-byte units of P per thread
+  const int t = threadIdx.x, lane = t & 63, wid = t >> 6;
   {
+    float4 pv[PV];
 #pragma unroll
-    for (int i = 0; i < QpackRegs<L, NT>::PV; ++i) {
-      const int e = 4 * (i * NT + threadIdx.x);
-      const int row = e >> 7, d = e & 127;
-      float* dst = &sh.P_s[row][d >> 5][d & 31];
-      dst[0] = r.pv[i].x, dst[1] = r.pv[i].y, dst[2] = r.pv[i].z, dst[3] = r.pv[i].w;
+    for (int r = 0; r < PV; ++r) pv[r] = reinterpret_cast<const float4*>(Pbh)[t + NT * r];
+    uint4 qv = make_uint4(0u, 0u, 0u, 0u);
+    if (t < G * (kHeadDim / 8)) qv = reinterpret_cast<const uint4*>(qg)[t];
+#pragma unroll
+    for (int r = 0; r < PV; ++r) {
+      const int f = t + NT * r;  // unit f of P: row f / 32, block (f / 8) mod 4, unit f mod 8
+      const int i = f >> 5, c = (f >> 3) & 3, u = f & 7;
+      sh.P[i * 32 + c * 8 + (u ^ qpack_swz(i, c))] = pv[r];
     }
+    if (t < G * (kHeadDim / 8)) sh.q[t / (kHeadDim / 8)][t % (kHeadDim / 8)] = qv;
+  }
+  __syncthreads();
+  BPC_STAMP(1, 6);
+  double xb = 0.0;  // the group sum of row t / 4 (every lane of the quad)
+  if (t < 4 * L) {  // whole wavefronts (4 L is a multiple of 64)
+    const int i = t >> 2, c = t & 3;
+    // four heads at a time: four independent fixed-order chains interleave;
+    // P is re-read from LDS eight coordinates at a time (held whole, as 32
+    // values, it would not fit beside the accumulators)
+    for (int g0 = 0; g0 < G; g0 += 4) {
+      double acc[4] = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll 1
+      for (int j = 0; j < 4; ++j) {
+        const float4 pa = sh.P[i * 32 + c * 8 + ((2 * j) ^ qpack_swz(i, c))];
+        const float4 pb = sh.P[i * 32 + c * 8 + ((2 * j + 1) ^ qpack_swz(i, c))];
+        const float pf[8] = {pa.x, pa.y, pa.z, pa.w, pb.x, pb.y, pb.z, pb.w};
+        uint32_t w4[4][4];
 #pragma unroll
-    for (int i = 0; i < QpackRegs<L, NT>::QV; ++i) {
-      const int e8 = i * NT + threadIdx.x;
-      if (e8 < G * kHeadDim / 8) {
-        const int e = 8 * e8;
-        const int g = e >> 7, d = e & 127;
-        float* dst = &sh.q_s[g][d >> 5][d & 31];
-        const uint32_t w[4] = {r.qv[i].x, r.qv[i].y, r.qv[i].z, r.qv[i].w};
+        for (int hh = 0; hh < 4; ++hh) {
+          // coordinates 32 c + 8 j .. 32 c + 8 j + 7 of head g0 + hh (a head
+          // past G reads head g0, whose result is dropped)
+          const uint4 qq = sh.q[g0 + hh < G ? g0 + hh : g0][4 * c + j];
+          w4[hh][0] = qq.x, w4[hh][1] = qq.y, w4[hh][2] = qq.z, w4[hh][3] = qq.w;
+        }
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          dst[2 * j] = bf16_to_f32(w[j] & 0xFFFFu);
-          dst[2 * j + 1] = bf16_to_f32(w[j] >> 16);
+        for (int e = 0; e < 4; ++e) {
+          const double d0 = (double)pf[2 * e], d1 = (double)pf[2 * e + 1];
+#pragma unroll
+          for (int hh = 0; hh < 4; ++hh) {
+            acc[hh] = __builtin_fma(d0, (double)bf16_to_f32(w4[hh][e] & 0xFFFFu), acc[hh]);
+            acc[hh] = __builtin_fma(d1, (double)bf16_to_f32(w4[hh][e] >> 16), acc[hh]);
+          }
         }
       }
-    }
-  }
-  __syncthreads();
-  const int ntriples = G * L * 4;
-  for (int base = 0; base < ntriples; base += NT) {
-    const int tr = base + threadIdx.x;
-    const bool valid = tr < ntriples;
-    const int c = tr & 3, gi = valid ? (tr >> 2) : 0;
-    const int g = gi / L, i = gi % L;
-    // each product of a bf16 query coordinate and an fp32 entry of P is
-    // exact in fp64 (8 + 24 significant bits), so the fused multiply-add
-    // rounds exactly as the separately rounded multiply and add would
-    double acc = 0.0;
-#pragma unroll 8
-    for (int e = 0; e < 32; ++e) acc = __builtin_fma((double)sh.P_s[i][c][e], (double)sh.q_s[g][c][e], acc);
-    const double s01 = dadd(acc, __shfl_xor(acc, 1, 64));
-    const double a = dadd(s01, __shfl_xor(s01, 2, 64));
-    if (valid && c == 0) sh.x_s[g][i] = a;
-  }
-  __syncthreads();
-  if (threadIdx.x < L) {
-    double x = sh.x_s[0][threadIdx.x];
-    for (int g = 1; g < G; ++g) x = dadd(x, sh.x_s[g][threadIdx.x]);
-    sh.xbar_s[threadIdx.x] = x;
-  }
-  __syncthreads();
-  if (threadIdx.x < 64) {
-    double m = 0.0;
-    for (int i = threadIdx.x; i < L; i += 64) m = fmax(m, fabs(sh.xbar_s[i]));
 #pragma unroll
-    for (int o = 1; o < 64; o <<= 1) m = fmax(m, __shfl_xor(m, o, 64));
-    if (threadIdx.x == 0) sh.mx_s = m;
+      for (int hh = 0; hh < 4; ++hh) {
+        // ((b0 + b1) + (b2 + b3)) on every lane of the quad
+        const double s01 = dadd(acc[hh], dpp_f64<kDppQuadXor1>(acc[hh]));
+        const double a = dadd(s01, dpp_f64<kDppQuadXor2>(s01));
+        if (g0 + hh < G) xb = (g0 + hh == 0) ? a : dadd(xb, a);
+      }
+    }
+    // max |xbar| of the wavefront: the quads are uniform, so two mirrors
+    // give the maximum of 16 lanes, and four read-lanes that of the wavefront
+    double m = fabs(xb);
+    m = fmax(m, dpp_f64<kDppHalfMirror>(m));
+    m = fmax(m, dpp_f64<kDppMirror>(m));
+    const int mlo = __double2loint(m), mhi = __double2hiint(m);
+    auto rl = [&](int l) {
+      return __hiloint2double(__builtin_amdgcn_readlane(mhi, l), __builtin_amdgcn_readlane(mlo, l));
+    };
+    m = fmax(fmax(rl(0), rl(16)), fmax(rl(32), rl(48)));
+    if (lane == 0) o.wmax[wid] = m;
   }
   __syncthreads();
-  const double m = sh.mx_s;
-  if (threadIdx.x < 128) {  // waves 0 and 1 cover i < L <= 128
-    const int i = threadIdx.x;
-    int p = 0;
-    if (i < L && m > 0.0) p = (int)round(dmul(sh.xbar_s[i], 127.0) / m);
+  BPC_STAMP(1, 7);
+  if (t < 4 * L) {
+    double m = o.wmax[0];
+#pragma unroll
+    for (int w = 1; w < 4 * L / 64; ++w) m = fmax(m, o.wmax[w]);
+    const int p = (m > 0.0) ? (int)round(dmul(xb, 127.0) / m) : 0;
     const uint32_t mag = (uint32_t)abs(p);
-    const int wid = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    // every quad holds one row: each plane's ballot has its bits at lanes 4 k
 #pragma unroll
     for (int plane = 0; plane < 8; ++plane) {
-      const bool on = (i < L) && (plane == 0 ? (p >= 0) : (((mag >> (plane - 1)) & 1u) != 0u));
-      const unsigned long long mask = __ballot(on);
-      if (lane < 2 && 2 * wid + lane < W) qc[plane * W + 2 * wid + lane] = (uint32_t)(mask >> (32 * lane));
+      const bool on = plane == 0 ? (p >= 0) : (((mag >> (plane - 1)) & 1u) != 0u);
+      const uint32_t piece = every_fourth_bit(__ballot(on));  // rows 16 wid .. 16 wid + 15
+      if (lane == 0) o.qc16[plane * (L / 16) + wid] = (uint16_t)piece;
     }
-    int s = (int)mag;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) s += __shfl_xor(s, o, 64);
-    if (lane == 0) sh.tsum_s[wid] = s;
   }
   __syncthreads();
-  if (threadIdx.x == 0) *T = sh.tsum_s[0] + sh.tsum_s[1];
-  __syncthreads();
-}
-
-// one 1024-thread workgroup per (b, h): the query planes and sum |p| go to
-// the workspace (and to qcode_out when given)
-template <int L>
-__global__ __launch_bounds__(kScanThreads) void qpack_kernel(const uint16_t* __restrict__ q,
-                                                            const float* __restrict__ P, int64_t sP_b, int64_t sP_h,
-                                                            int Hkv, int G, uint32_t* __restrict__ qcode_ws,
-                                                            uint32_t* __restrict__ qcode_out) {
-  constexpr int W = L / 32;
-  __shared__ QpackShared<L> sh;
-  __shared__ uint32_t qc_s[8 * W];
-  __shared__ int T_s;
-  const int bh = blockIdx.x;
-  BPC_STAMP(0, 0);
-  QpackRegs<L, kScanThreads> qr;
-  qpack_load<L, kScanThreads>(qr, q, P, sP_b, sP_h, Hkv, G, bh);
-  qpack_body<L, kScanThreads>(sh, qr, G, qc_s, &T_s);
-  // per (b, h): 8 W plane words, then sum |p|
-  uint32_t* dst = qcode_ws + (size_t)bh * kQcodeStride;
-  if (threadIdx.x < 8 * W) {
-    dst[threadIdx.x] = qc_s[threadIdx.x];
-    if (qcode_out) qcode_out[(size_t)bh * 8 * W + threadIdx.x] = qc_s[threadIdx.x];
-  }
-  if (threadIdx.x == 0) dst[8 * W] = (uint32_t)T_s;
-  BPC_STAMP(0, 1);
 }
 
 // ---------------------------------------------------------------------------
-// 1. score -- one 1024-thread workgroup per slice.
-// Each thread scores 16 keys with 16-byte non-temporal loads, in two rounds
-// whose loads are all issued before the first is consumed (the first round
-// is in flight while the query is packed), and keeps their distances in
-// registers, two per register; the slice histogram lives in LDS.
+// 1. score -- one 512-thread workgroup per slice.
+// The workgroup first packs its (b, h)'s query group (above).  Each thread
+// then scores 32 keys with 16-byte non-temporal loads (a ring of kScanRing
+// loads in flight) and keeps their distances in registers, two per
+// register; the slice histogram lives in LDS.
 // ---------------------------------------------------------------------------
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 constexpr int kScanRing = 4;  // 16-byte code loads in flight per thread
@@ -273,7 +273,9 @@ struct ScoreShared {
   static constexpr int NBP = (NB + 127) & ~127;  // histogram padded to whole coarse bins
   union U {
     uint32_t hist[NBP];
+    QpackShared<L> qp;  // the query packing, before the histogram is cleared
   } u;
+  QpackOut<L> qo;
   uint32_t coarse[kCoarseBins];
   uint32_t cc[kCoarseBins + 1];
   int cnt[128];
@@ -283,7 +285,9 @@ struct ScoreShared {
 // FULL: the slice holds kSlice keys and its codes are 16-byte aligned, so no
 // per-key bounds tests are needed and every load is one 16-byte load
 template <int L, bool FULL>
-__device__ __forceinline__ void score_body(ScoreShared<L>& sh, int bh, int s, const uint32_t* __restrict__ qcode_ws,
+__device__ __forceinline__ void score_body(ScoreShared<L>& sh, int bh, int s, const uint16_t* __restrict__ q,
+                                           const float* __restrict__ P, int64_t sP_b, int64_t sP_h, int G,
+                                           uint32_t* __restrict__ qcode_ws, uint32_t* __restrict__ qcode_out,
                                            const uint32_t* __restrict__ codes, int64_t sC_b, int64_t sC_h, int Hkv,
                                            int N, int k, int nslices, uint32_t* __restrict__ cand,
                                            uint32_t* __restrict__ meta, uint32_t* __restrict__ hist_fine,
@@ -323,20 +327,36 @@ __device__ __forceinline__ void score_body(ScoreShared<L>& sh, int bh, int s, co
       return load_code_group<W>(cb, n, cnt, vec_ok);
   };
 
-  // the query planes (uniform: scalar loads) and round 0 of the code loads
-  const uint32_t* qc = qcode_ws + (size_t)bh * kQcodeStride;
+  // the query planes of (b, h), packed before any code load is issued; they
+  // are uniform (scalar registers).  Slice 0 also stores them (and sum |p|)
+  // for the attention kernel and the caller.
+  qpack_block<L, NT>(sh.u.qp, sh.qo, q + ((size_t)b * Hkv * G + (size_t)h * G) * kHeadDim, P + b * sP_b + h * sP_h,
+                     G);
+  BPC_STAMP(1, 5);
+  const uint32_t* qcw = reinterpret_cast<const uint32_t*>(sh.qo.qc16);
   uint32_t sg[W], M[7][W];
+  int T = 0;  // sum |p_i| = sum_j 2^j popcount(plane 1 + j)
 #pragma unroll
   for (int w = 0; w < W; ++w) {
-    sg[w] = qc[w];
+    sg[w] = __builtin_amdgcn_readfirstlane(qcw[w]);
 #pragma unroll
-    for (int j = 0; j < 7; ++j) M[j][w] = qc[(1 + j) * W + w];
+    for (int j = 0; j < 7; ++j) {
+      M[j][w] = __builtin_amdgcn_readfirstlane(qcw[(1 + j) * W + w]);
+      T += __popc(M[j][w]) << j;
+    }
   }
   // a ring of RD code loads per thread stays in flight: the load of group
   // it + RD is issued as soon as group it has been consumed
   u32x4_t cw[RD];
 #pragma unroll
   for (int r = 0; r < RD; ++r) cw[r] = load_group(r);
+  if (s == 0 && threadIdx.x <= 8 * W) {
+    const uint32_t v = threadIdx.x < 8 * W ? qcw[threadIdx.x] : (uint32_t)T;
+    qcode_ws[(size_t)bh * kQcodeStride + threadIdx.x] = v;
+    if (qcode_out && threadIdx.x < 8 * W) qcode_out[(size_t)bh * 8 * W + threadIdx.x] = v;
+  }
+  // the packing's LDS area is dead: every thread has passed the barrier
+  // that ends qpack_block
 #pragma unroll
   for (int r = 0; r < NBP / NT; ++r) sh.u.hist[r * NT + threadIdx.x] = 0u;
   __syncthreads();
@@ -561,7 +581,6 @@ __device__ __forceinline__ void score_body(ScoreShared<L>& sh, int bh, int s, co
   }
   if (threadIdx.x == 0) *reinterpret_cast<uint4*>(meta + sl * 4) = make_uint4(kth, cmin, sh.total, cand_max);
   if (score_out) {  // debug output
-    const int T = (int)qc[8 * W];
     int32_t* so = score_out + (size_t)bh * N + n0;
 #pragma unroll
     for (int it = 0; it < NLD; ++it)
@@ -581,7 +600,9 @@ __device__ __forceinline__ void score_body(ScoreShared<L>& sh, int bh, int s, co
 // is only launched when such slices exist.
 template <int L, bool FULL>
 __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(L <= 64 ? 8 : 4))) void score_kernel(
-    const uint32_t* __restrict__ qcode_ws, const uint32_t* __restrict__ codes, int64_t sC_b, int64_t sC_h, int BH,
+    const uint16_t* __restrict__ q, const float* __restrict__ P, int64_t sP_b, int64_t sP_h, int G,
+    uint32_t* __restrict__ qcode_ws, uint32_t* __restrict__ qcode_out, const uint32_t* __restrict__ codes,
+    int64_t sC_b, int64_t sC_h, int BH,
     int Hkv, int N, int k, int nslices, uint32_t* __restrict__ cand, uint32_t* __restrict__ meta,
     uint32_t* __restrict__ hist_fine, uint32_t* __restrict__ hist_cc, uint32_t* __restrict__ win,
     int32_t* __restrict__ score_out) {
@@ -592,7 +613,7 @@ __global__ __launch_bounds__(kScoreThreads) __attribute__((amdgpu_waves_per_eu(L
   const bool full = (s + 1) * kSlice <= N && (reinterpret_cast<uintptr_t>(codes + c0) & 15u) == 0;
   if (full != FULL) return;
   BPC_STAMP(1, 0);
-  score_body<L, FULL>(sh, bh, s, qcode_ws, codes, sC_b, sC_h, Hkv, N, k, nslices, cand, meta, hist_fine, hist_cc,
+  score_body<L, FULL>(sh, bh, s, q, P, sP_b, sP_h, G, qcode_ws, qcode_out, codes, sC_b, sC_h, Hkv, N, k, nslices, cand, meta, hist_fine, hist_cc,
                       win, score_out);
   BPC_STAMP(1, 4);
 }
@@ -653,7 +674,7 @@ struct AttendShared {
     uint32_t fine[kPlanCache][1 << kCoarseShift];  // fine bins of c* of each slice
     int kth[kPlanCache], cmin[kPlanCache];
   };
-  union U {
+  union alignas(16) U {
     Plan plan;
     uint32_t win[kWinSlices][kWinRec];  // one-round threshold: the window records of the slices
     int rows[kRowCache];                // the slice's selected keys, ascending
@@ -662,10 +683,9 @@ struct AttendShared {
   float st[kAttnWaves][G][2];  // per wavefront (max, sum)
   alignas(16) float pl[kAttnWaves][G][16];  // per wavefront: the logits of a pass, handed between lanes
   uint4 q[G][kHeadDim / 8];     // the group's queries, bf16
-  int wave_tot[kAttnWaves];
+  int wave_tot[2][kAttnWaves];  // block scans, double-buffered
   int first[2];
   int red[2][kAttnWaves];
-  int plan3[3];               // one-round threshold: take, off, kept of this slice
   uint32_t sel[kSlice / 32];  // the safeguard: bitmap of the slice's keys the hash selection took
 };
 
@@ -675,8 +695,10 @@ __device__ __forceinline__ void pin_regs(uint4& x) {
   __asm__ volatile("" : "+v"(x.x), "+v"(x.y), "+v"(x.z), "+v"(x.w));
 }
 
-// One pass of a wavefront over nrows (1..kAttnRows) rows; lane l < nrows
-// holds the key index of row l in myidx; pl is the wavefront's [G][16] LDS
+// One pass of a wavefront over nrows (1..kAttnRows) rows; lane (r, c) =
+// (lane / 16, lane % 16) holds the key index of row c in rk and those of
+// rows 4 r .. 4 r + 3 in rv (key 0 for a row at or past nrows: it exists in
+// every head, and its logit is masked); pl is the wavefront's [G][16] LDS
 // area for the logits.  Updates the wavefront's running maximum Mx and sum
 // Ls (uniform over the wavefront) and this lane's weighted-V partials o.
 //
@@ -688,20 +710,13 @@ __device__ __forceinline__ void pin_regs(uint4& x) {
 // dims [8 c, 8 c + 8) of rows 4 r .. 4 r + 3, which are exactly the rows
 // whose logits the lanes (r, head < G) of its own group hold.
 template <int G>
-__device__ __forceinline__ void attend_pass(int myidx, int nrows, const uint4 (*qs)[kHeadDim / 8], float (*pl)[16],
-                                            const char* Kh, uint32_t kstride, const char* Vh, uint32_t vstride,
-                                            float scale_log2, float (&Mx)[G], float (&Ls)[G], float (&o)[G][8]) {
+__device__ __forceinline__ void attend_pass(uint32_t rk, const uint32_t (&rv)[4], int nrows,
+                                            const uint4 (*qs)[kHeadDim / 8], float (*pl)[16], const char* Kh,
+                                            uint32_t kstride, const char* Vh, uint32_t vstride, float scale_log2,
+                                            float (&Mx)[G], float (&Ls)[G], float (&o)[G][8]) {
   static_assert(G <= 16, "the query heads of a group fill at most the 16 columns of a tile");
   const int lane = threadIdx.x & 63;
   const int c16 = lane & 15, r4 = lane >> 4;
-  const uint32_t nk = (uint32_t)__shfl(myidx, c16, 64);
-  const uint32_t rk = c16 < nrows ? nk : 0u;  // row 0 of the head always exists
-  uint32_t rv[4];
-#pragma unroll
-  for (int t = 0; t < 4; ++t) {
-    const uint32_t n = (uint32_t)__shfl(myidx, 4 * r4 + t, 64);
-    rv[t] = 4 * r4 + t < nrows ? n : 0u;
-  }
   uint4 kv[4], vv[4];
 #pragma unroll
   for (int kb = 0; kb < 4; ++kb) kv[kb] = *reinterpret_cast<const uint4*>(Kh + (rk * kstride + 64u * kb + 16u * r4));
@@ -790,10 +805,13 @@ __device__ __forceinline__ void write_partial(float (&o_s)[kAttnWaves][G][kHeadD
   for (int g = 0; g < G; ++g)
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      float x = o[g][e];
-      x += __shfl_xor(x, 16, 64);
-      x += __shfl_xor(x, 32, 64);
-      o[g][e] = x;
+      // x[l] + x[l ^ 16], then + the same over l ^ 32: with both operands
+      // equal, the two results of a permlane swap sum to exactly that
+      const uint32_t x = __float_as_uint(o[g][e]);
+      const auto p16 = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+      const uint32_t y = __float_as_uint(__uint_as_float(p16[0]) + __uint_as_float(p16[1]));
+      const auto p32 = __builtin_amdgcn_permlane32_swap(y, y, false, false);
+      o[g][e] = __uint_as_float(p32[0]) + __uint_as_float(p32[1]);
     }
   if (lane < 16) {
 #pragma unroll
@@ -895,6 +913,7 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(G 
     for (int r = 0; r < RV; ++r) pin_regs(wv[r]);
     pin_regs(qv);
     if (threadIdx.x < G * kHeadDim / 8) sh.q[threadIdx.x / (kHeadDim / 8)][threadIdx.x % (kHeadDim / 8)] = qv;
+    BPC_STAMP(2, 1);
     uint4* wdst = reinterpret_cast<uint4*>(&sh.u.win[0][0]);
 #pragma unroll
     for (int r = 0; r < RV; ++r)
@@ -908,53 +927,42 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(G 
     };
     int lo = 0, hi = 1 << 30;
     for (int u = 0; u < nslices; ++u) lo = max(lo, (int)sh.u.win[u][0]), hi = min(hi, (int)sh.u.win[u][1]);
-    int below = 0, bad = lo > hi;
-    const int t = lo - 1 + (int)threadIdx.x;  // hi - lo + 2 <= kWinBins + 1 <= kAttnThreads values
-    if (!bad && t <= hi) {
+    // thread i evaluates S(t) at t = lo - 1 + i (hi - lo + 2 <= kWinBins + 1 <= kAttnThreads values); the
+    // counts of t in [lo, hi] with S(t) < k and the failed checks go through ballots
+    bool below = false, badt = false;
+    const int t = lo - 1 + (int)threadIdx.x;
+    if (lo <= hi && t <= hi) {
       int St = 0;
       for (int u = 0; u < nslices; ++u) St += cum(u, t);
       if (t == lo - 1)
-        bad = St >= k;
+        badt = St >= k;
       else
         below = St < k;
-      if (t == hi && St < k) bad = 1;
+      if (t == hi && St < k) badt = true;
     }
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) below += __shfl_xor(below, o, 64), bad |= __shfl_xor(bad, o, 64);
-    if (lane == 0) sh.red[0][wid] = below, sh.red[1][wid] = bad;
+    const unsigned long long mbelow = __ballot(below), mbad = __ballot(badt);
+    if (lane == 0) sh.red[0][wid] = (int)__popcll(mbelow), sh.red[1][wid] = mbad != 0ull;
     __syncthreads();
-    int cntlow = 0;
-    bad = 0;
+    BPC_STAMP(2, 2);
+    int cntlow = 0, bad = lo > hi;
 #pragma unroll
     for (int w = 0; w < kAttnWaves; ++w) cntlow += sh.red[0][w], bad |= sh.red[1][w];
     if (!bad) {
       tstar = lo + cntlow;
-      // keys below T* and ties at T*, per slice (wavefront 0, lane u = slice
-      // u); ties go to the lowest indices, i.e. slice by slice
-      if (wid == 0) {
-        int bu = 0, tu = 0;
-        if (lane < nslices) {
-          bu = cum(lane, tstar - 1);
-          tu = cum(lane, tstar) - bu;
-        }
-        int bi = bu, ti = tu;  // inclusive prefix over slices
-#pragma unroll
-        for (int o = 1; o < 64; o <<= 1) {
-          const int yb = __shfl_up(bi, o, 64), yt = __shfl_up(ti, o, 64);
-          if (lane >= o) bi += yb, ti += yt;
-        }
-        const int below_all = __shfl(bi, 63, 64);
-        if (lane == s) {
-          const int need = k - below_all;  // keys at T* to take, over all slices
-          const int below_before = bi - bu, ties_before = ti - tu;
-          const int tk = max(0, min(tu, need - ties_before));
-          sh.plan3[0] = tk;
-          sh.plan3[1] = below_before + min(need, ties_before);
-          sh.plan3[2] = bu + tk;
-        }
+      // every thread derives its slice's plan from the windows: keys below T*
+      // and ties at T* per slice; ties go to the lowest indices, i.e. the
+      // slices before s take min(need, their ties) of the `need` ties
+      int below_all = 0, below_before = 0, ties_before = 0, bs = 0, ts = 0;
+      for (int u = 0; u < nslices; ++u) {
+        const int bu = cum(u, tstar - 1), tu = cum(u, tstar) - bu;
+        below_all += bu;
+        if (u < s) below_before += bu, ties_before += tu;
+        if (u == s) bs = bu, ts = tu;
       }
-      __syncthreads();
-      take = sh.plan3[0], off = sh.plan3[1], kept = sh.plan3[2];
+      const int need = k - below_all;  // keys at T* to take, over all slices
+      take = max(0, min(ts, need - ties_before));
+      off = below_before + min(need, ties_before);
+      kept = bs + take;
       planned = true;
     }
     __syncthreads();  // the window area is reused below
@@ -1138,6 +1146,7 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(G 
     }
   };
   int nkept = 0, tie_seen = 0;  // kept keys and ties at T* in earlier batches
+  int sbuf = 0;                 // block scans alternate their LDS totals
   for (int base = 0; base < nent; base += kCandBatch) {
     if (!planned)
       rescore(base);
@@ -1154,7 +1163,8 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(G 
     }
     int tot;
     // one scan of packed (ties << 16 | below): at most kCandBatch of each per batch
-    const int pre = block_exclusive_scan<kAttnThreads>((nt << 16) | nb, sh.wave_tot, tot);
+    const int pre = block_exclusive_scan_bits<kAttnThreads, 0x70007u>((nt << 16) | nb, sh.wave_tot, sbuf, tot);
+    sbuf ^= 1;
     int tie_rank = tie_seen + (pre >> 16);
     int rank = nkept + (pre & 0xFFFF) + max(0, min(tie_rank, take) - min(tie_seen, take));
 #pragma unroll
@@ -1201,7 +1211,8 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(G 
         na += add[u];
       }
       int tot;
-      int pos = kept + extra + block_exclusive_scan<kAttnThreads>(na, sh.wave_tot, tot);
+      int pos = kept + extra + block_exclusive_scan_bits<kAttnThreads, 0x7u>(na, sh.wave_tot, sbuf, tot);
+      sbuf ^= 1;
 #pragma unroll
       for (int u = 0; u < 4; ++u)
         if (add[u]) {
@@ -1229,15 +1240,32 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(G 
 #pragma unroll
     for (int e = 0; e < 8; ++e) o[g][e] = 0.f;
   }
+  // lane (r, c) reads the key indices of row c and rows 4 r .. 4 r + 3 of
+  // the pass from the row list (entries at or past kept are masked; the
+  // list's area holds r0 + 15 since r0 is a multiple of 16 below kept)
+  auto pass_rows = [&](const int32_t* rl, int r0, int nr, uint32_t& rk, uint32_t (&rv)[4]) {
+    const int c16 = lane & 15, r4 = lane >> 4;
+    const int kc = rl[r0 + c16];
+    const int4 v4 = *reinterpret_cast<const int4*>(rl + r0 + 4 * r4);
+    rk = c16 < nr ? (uint32_t)kc : 0u;
+    rv[0] = 4 * r4 + 0 < nr ? (uint32_t)v4.x : 0u;
+    rv[1] = 4 * r4 + 1 < nr ? (uint32_t)v4.y : 0u;
+    rv[2] = 4 * r4 + 2 < nr ? (uint32_t)v4.z : 0u;
+    rv[3] = 4 * r4 + 3 < nr ? (uint32_t)v4.w : 0u;
+  };
   if (rows_lds) {
     for (int r0 = wid * kAttnRows; r0 < kept; r0 += kAttnWaves * kAttnRows) {
       const int nr = min(kAttnRows, kept - r0);
-      attend_pass<G>(lane < nr ? sh.u.rows[r0 + lane] : 0, nr, sh.q, sh.pl[wid], Kh, kstride, Vh, vstride, scale_log2, Mx, Ls, o);
+      uint32_t rk, rv[4];
+      pass_rows(sh.u.rows, r0, nr, rk, rv);
+      attend_pass<G>(rk, rv, nr, sh.q, sh.pl[wid], Kh, kstride, Vh, vstride, scale_log2, Mx, Ls, o);
     }
   } else {
     for (int r0 = wid * kAttnRows; r0 < kept; r0 += kAttnWaves * kAttnRows) {
       const int nr = min(kAttnRows, kept - r0);
-      attend_pass<G>(lane < nr ? grows[r0 + lane] : 0, nr, sh.q, sh.pl[wid], Kh, kstride, Vh, vstride, scale_log2, Mx, Ls, o);
+      uint32_t rk, rv[4];
+      pass_rows(grows, r0, nr, rk, rv);
+      attend_pass<G>(rk, rv, nr, sh.q, sh.pl[wid], Kh, kstride, Vh, vstride, scale_log2, Mx, Ls, o);
     }
   }
   BPC_STAMP(2, 5);
@@ -1292,7 +1320,12 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(G 
   }
   for (int r0 = wid * kAttnRows; r0 < cnt; r0 += kAttnWaves * kAttnRows) {
     const int nr = min(kAttnRows, cnt - r0);
-    attend_pass<G>(lane < nr ? n0 + r0 + lane : 0, nr, sh.q, sh.pl[wid], Kh, kstride, Vh, vstride, scale_log2, Mx, Ls, o);
+    const int c16 = lane & 15, r4 = lane >> 4;
+    const uint32_t rk = c16 < nr ? (uint32_t)(n0 + r0 + c16) : 0u;
+    uint32_t rv[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) rv[t] = 4 * r4 + t < nr ? (uint32_t)(n0 + r0 + 4 * r4 + t) : 0u;
+    attend_pass<G>(rk, rv, nr, sh.q, sh.pl[wid], Kh, kstride, Vh, vstride, scale_log2, Mx, Ls, o);
   }
   write_partial<G>(sh.o, sh.st, Mx, Ls, o, part + (size_t)blockIdx.x * G * (kHeadDim + 2));
 }
@@ -1349,7 +1382,8 @@ __global__ __launch_bounds__(kHeadDim) void merge_kernel(int Hkv, int G, int nch
 }
 
 // ---------------------------------------------------------------------------
-// Launch sequence (all on the caller's stream): score -> attend -> merge.
+// Launch sequence (all on the caller's stream): score (with the query
+// packing) -> attend -> merge.
 // ---------------------------------------------------------------------------
 template <int L>
 static hipError_t launch_decode_L(const DecodeArgs& a, const DecodeLayout& lay) {
@@ -1371,16 +1405,16 @@ static hipError_t launch_decode_L(const DecodeArgs& a, const DecodeLayout& lay) 
   const int win_ok = lay.nslices <= kWinSlices;
 
   mark(0);
-  qpack_kernel<L><<<BH, kScanThreads, 0, st>>>(a.q, a.P, a.sP_b, a.sP_h, a.Hkv, lay.G, qcode, a.qcode_out);
-  mark(1);
-  score_kernel<L, true><<<nwg, kScoreThreads, 0, st>>>(qcode, a.codes, a.sC_b, a.sC_h, BH, a.Hkv, a.N, a.k,
-                                                     lay.nslices, cand, meta, hist_fine, hist_cc, win, a.score_out);
+  score_kernel<L, true><<<nwg, kScoreThreads, 0, st>>>(a.q, a.P, a.sP_b, a.sP_h, lay.G, qcode, a.qcode_out, a.codes,
+                                                     a.sC_b, a.sC_h, BH, a.Hkv, a.N, a.k, lay.nslices, cand, meta,
+                                                     hist_fine, hist_cc, win, a.score_out);
   // slices of the other kind: a ragged last slice, or codes whose head or
   // batch stride is not a multiple of four words (the base is 16-byte aligned)
   if (a.N % kSlice != 0 || (a.sC_b * 4) % 16 != 0 || (a.sC_h * 4) % 16 != 0)
-    score_kernel<L, false><<<nwg, kScoreThreads, 0, st>>>(qcode, a.codes, a.sC_b, a.sC_h, BH, a.Hkv, a.N, a.k,
-                                                          lay.nslices, cand, meta, hist_fine, hist_cc, win, a.score_out);
-  mark(2);
+    score_kernel<L, false><<<nwg, kScoreThreads, 0, st>>>(a.q, a.P, a.sP_b, a.sP_h, lay.G, qcode, a.qcode_out,
+                                                          a.codes, a.sC_b, a.sC_h, BH, a.Hkv, a.N, a.k, lay.nslices,
+                                                          cand, meta, hist_fine, hist_cc, win, a.score_out);
+  mark(1);
   switch (lay.G) {
 #define BPC_ATTEND_CASE(GG)                                                                                     \
   case GG:                                                                                                      \
@@ -1399,9 +1433,9 @@ static hipError_t launch_decode_L(const DecodeArgs& a, const DecodeLayout& lay) 
     default:
       break;
   }
-  mark(3);
+  mark(2);
   merge_kernel<<<a.B * a.Hq, kHeadDim, 0, st>>>(a.Hkv, lay.G, lay.nslices, part, a.out);
-  mark(4);
+  mark(3);
   return hipGetLastError();
 }
 
