@@ -189,6 +189,37 @@ __device__ __forceinline__ int block_exclusive_scan(int v, int* wave_tot, int& t
 
 // lowest set lane of a 64-bit ballot, or 64
 // ---------------------------------------------------------------------------
+// wavefront scans on DPP (no LDS round trips): within each row of 16 lanes
+// by shifts of 1, 2, 4 and 8, then across rows with the broadcasts of lanes
+// 15 and 31 (gfx9 DPP row_shr / row_bcast)
+// ---------------------------------------------------------------------------
+template <int CTRL, int ROWS = 0xF>
+__device__ __forceinline__ int dpp_or_zero(int x) {
+  return __builtin_amdgcn_update_dpp(0, x, CTRL, ROWS, 0xF, false);
+}
+// inclusive prefix sum over the 64 lanes
+__device__ __forceinline__ int wave_inclusive_sum(int x) {
+  x += dpp_or_zero<0x111>(x);        // row_shr:1
+  x += dpp_or_zero<0x112>(x);        // row_shr:2
+  x += dpp_or_zero<0x114>(x);        // row_shr:4
+  x += dpp_or_zero<0x118>(x);        // row_shr:8
+  x += dpp_or_zero<0x142, 0xA>(x);   // row_bcast:15 into rows 1 and 3
+  x += dpp_or_zero<0x143, 0xC>(x);   // row_bcast:31 into rows 2 and 3
+  return x;
+}
+// inclusive prefix sum within each group of 8 consecutive lanes
+__device__ __forceinline__ int group8_inclusive_sum(int x) {
+  const int part = threadIdx.x & 7;
+  int y = dpp_or_zero<0x111>(x);
+  x += (part >= 1) ? y : 0;
+  y = dpp_or_zero<0x112>(x);
+  x += (part >= 2) ? y : 0;
+  y = dpp_or_zero<0x114>(x);
+  x += (part >= 4) ? y : 0;
+  return x;
+}
+
+// ---------------------------------------------------------------------------
 // block-wide exclusive scan of one non-negative int per thread whose set
 // bits all lie in MASK, without cross-lane shuffles: within a wavefront the
 // prefix is sum_b 2^b * (lanes below with bit b set), one ballot and one

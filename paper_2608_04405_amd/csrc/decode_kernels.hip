@@ -412,12 +412,7 @@ __device__ __forceinline__ void score_body(ScoreShared<L>& sh, int bh, int s, co
     int local = 0;
 #pragma unroll
     for (int e = 0; e < 16; ++e) local += (int)cntv[e];
-    int incl = local;
-#pragma unroll
-    for (int o = 1; o < 8; o <<= 1) {
-      const int y = __shfl_up(incl, o, 64);
-      if (part >= o) incl += y;
-    }
+    const int incl = group8_inclusive_sum(local);
     if (part == 7) sh.coarse[cbin] = (uint32_t)incl;
     if (fb0 < NBP) {
       uint32_t run = (uint32_t)(incl - local);
@@ -443,12 +438,7 @@ __device__ __forceinline__ void score_body(ScoreShared<L>& sh, int bh, int s, co
   const int mloc = (int)(((int64_t)k * cnt + N - 1) / N);
   if (threadIdx.x < 64) {
     const uint32_t c0 = sh.coarse[2 * lane], c1 = sh.coarse[2 * lane + 1];
-    int x = (int)(c0 + c1);
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const int y = __shfl_up(x, o, 64);
-      if (lane >= o) x += y;
-    }
+    const int x = wave_inclusive_sum((int)(c0 + c1));
     const int ex = x - (int)(c0 + c1);
     sh.cc[2 * lane] = (uint32_t)ex;
     sh.cc[2 * lane + 1] = (uint32_t)ex + c0;
@@ -540,9 +530,8 @@ __device__ __forceinline__ void score_body(ScoreShared<L>& sh, int bh, int s, co
     for (int it = 0; it < NLD; ++it)
 #pragma unroll
       for (int u = 0; u < KPL; ++u) c += is_cand(it, u, cand_max) ? 1 : 0;
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) c += __shfl_xor(c, o, 64);
-    if (lane == 0) sh.cnt[wid] = c;
+    c = wave_inclusive_sum(c);  // lane 63: the wavefront's count
+    if (lane == 63) sh.cnt[wid] = c;
   }
   // the write pass re-derives its flags instead of keeping PER comparison masks
 #pragma unroll
@@ -550,12 +539,7 @@ __device__ __forceinline__ void score_body(ScoreShared<L>& sh, int bh, int s, co
   __syncthreads();
   if (threadIdx.x < 64) {
     const int v = (lane < NW) ? sh.cnt[lane] : 0;
-    int x = v;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const int y = __shfl_up(x, o, 64);
-      if (lane >= o) x += y;
-    }
+    const int x = wave_inclusive_sum(v);
     if (lane < NW) sh.cnt[64 + lane] = x - v;
     if (lane == 63) sh.total = x;
   }
