@@ -207,6 +207,18 @@ __device__ __forceinline__ int wave_inclusive_sum(int x) {
   x += dpp_or_zero<0x143, 0xC>(x);   // row_bcast:31 into rows 2 and 3
   return x;
 }
+// maximum / minimum over the 64 lanes, in every lane: quad permutations and
+// row mirrors reduce each row of 16 lanes, read-lanes combine the four rows
+template <bool MAX>
+__device__ __forceinline__ int wave_reduce_maxmin(int x) {
+  auto op = [](int a, int b) { return MAX ? max(a, b) : min(a, b); };
+  x = op(x, __builtin_amdgcn_mov_dpp(x, 0xB1, 0xF, 0xF, false));   // quad_perm [1, 0, 3, 2]
+  x = op(x, __builtin_amdgcn_mov_dpp(x, 0x4E, 0xF, 0xF, false));   // quad_perm [2, 3, 0, 1]
+  x = op(x, __builtin_amdgcn_mov_dpp(x, 0x141, 0xF, 0xF, false));  // row_half_mirror
+  x = op(x, __builtin_amdgcn_mov_dpp(x, 0x140, 0xF, 0xF, false));  // row_mirror
+  return op(op(__builtin_amdgcn_readlane(x, 0), __builtin_amdgcn_readlane(x, 16)),
+            op(__builtin_amdgcn_readlane(x, 32), __builtin_amdgcn_readlane(x, 48)));
+}
 // inclusive prefix sum within each group of 8 consecutive lanes
 __device__ __forceinline__ int group8_inclusive_sum(int x) {
   const int part = threadIdx.x & 7;

@@ -909,14 +909,16 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(G 
       const uint32_t w = sh.u.win[u][4 + (max(j, 0) >> 1)];
       return (j < 0) ? (int)sh.u.win[u][2] : (int)((j & 1) ? (w >> 16) : (w & 0xFFFFu));
     };
-    int lo = 0, hi = 1 << 30;
-    for (int u = 0; u < nslices; ++u) lo = max(lo, (int)sh.u.win[u][0]), hi = min(hi, (int)sh.u.win[u][1]);
+    // lane u holds slice u's window (base, cand_max); lo and hi for every lane
+    const int lo = wave_reduce_maxmin<true>(lane < nslices ? (int)sh.u.win[lane][0] : 0);
+    const int hi = wave_reduce_maxmin<false>(lane < nslices ? (int)sh.u.win[lane][1] : (1 << 30));
     // thread i evaluates S(t) at t = lo - 1 + i (hi - lo + 2 <= kWinBins + 1 <= kAttnThreads values); the
     // counts of t in [lo, hi] with S(t) < k and the failed checks go through ballots
     bool below = false, badt = false;
     const int t = lo - 1 + (int)threadIdx.x;
     if (lo <= hi && t <= hi) {
       int St = 0;
+#pragma unroll 8
       for (int u = 0; u < nslices; ++u) St += cum(u, t);
       if (t == lo - 1)
         badt = St >= k;
@@ -933,16 +935,19 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(G 
     for (int w = 0; w < kAttnWaves; ++w) cntlow += sh.red[0][w], bad |= sh.red[1][w];
     if (!bad) {
       tstar = lo + cntlow;
-      // every thread derives its slice's plan from the windows: keys below T*
-      // and ties at T* per slice; ties go to the lowest indices, i.e. the
-      // slices before s take min(need, their ties) of the `need` ties
-      int below_all = 0, below_before = 0, ties_before = 0, bs = 0, ts = 0;
-      for (int u = 0; u < nslices; ++u) {
-        const int bu = cum(u, tstar - 1), tu = cum(u, tstar) - bu;
-        below_all += bu;
-        if (u < s) below_before += bu, ties_before += tu;
-        if (u == s) bs = bu, ts = tu;
+      // every wavefront derives its slice's plan from the windows, lane u for
+      // slice u: keys below T* and ties at T*, and their prefix sums over the
+      // slices; ties go to the lowest indices, i.e. the slices before s take
+      // min(need, their ties) of the `need` ties
+      int bu = 0, tu = 0;
+      if (lane < nslices) {
+        bu = cum(lane, tstar - 1);
+        tu = cum(lane, tstar) - bu;
       }
+      const int bi = wave_inclusive_sum(bu), ti = wave_inclusive_sum(tu);
+      const int below_all = __builtin_amdgcn_readlane(bi, 63);
+      const int below_before = __builtin_amdgcn_readlane(bi - bu, s), ties_before = __builtin_amdgcn_readlane(ti - tu, s);
+      const int bs = __builtin_amdgcn_readlane(bu, s), ts = __builtin_amdgcn_readlane(tu, s);
       const int need = k - below_all;  // keys at T* to take, over all slices
       take = max(0, min(ts, need - ties_before));
       off = below_before + min(need, ties_before);
