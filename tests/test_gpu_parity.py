@@ -281,7 +281,7 @@ def _random_case(rng, B, Hq, Hkv, N, L, Ncap=None, code_pool=None, qscale=1.0):
     dict(B=1, Hq=4, Hkv=2, N=1001, L=32, k=30),                   # last 16-byte group holds one key
     dict(B=2, Hq=4, Hkv=2, N=333, L=64, k=7, pool=5),             # odd key count, ties
     dict(B=1, Hq=8, Hkv=2, N=65537, L=64, k=1311),                # ragged second run
-    dict(B=1, Hq=2, Hkv=1, N=1100000, L=32, k=50000, pool=40),    # over a million keys: three-kernel path
+    dict(B=1, Hq=2, Hkv=1, N=1100000, L=32, k=50000, pool=40),    # over a million keys (68 slices): two-round threshold path
 ])
 def test_decode_edge_cases(case):
     announce(f"[decode edge] {case}")
