@@ -74,8 +74,9 @@ __device__ __forceinline__ void slice_tile(int id, int BH, int nslices, int& bh,
 // ---------------------------------------------------------------------------
 // Query projection, quantisation and packing (Sec. 3.2 "Retrieval Phase";
 // Appendix "Packing kernel"), done by every scoring workgroup for its own
-// (b, h) before its first code load, so that the loads of P and q are not
-// queued behind the code stream of other workgroups.  All slices of a
+// (b, h) before its code stream starts (one code load per thread goes out
+// behind the P loads), so that the loads of P and q are not queued behind
+// the code stream of other workgroups.  All slices of a
 // (b, h) run on one XCD: P and q come from HBM once, then from its L2.
 //
 // P is loaded with coalesced 16-byte loads and staged in LDS (in the place
@@ -130,11 +131,12 @@ __device__ __forceinline__ uint32_t every_fourth_bit(unsigned long long m) {
 }
 
 // The planes land in o.qc16 (read them as 8 W little-endian u32 words: plane
-// 0 = signs, plane 1 + j = bit j of |p|).  Ends with a barrier; sh is free
-// after it.
-template <int L, int NT>
+// 0 = signs, plane 1 + j = bit j of |p|).  after_loads() runs right after
+// the P and query loads are issued, so that the caller can put loads of its
+// own in flight behind them.  Ends with a barrier; sh is free after it.
+template <int L, int NT, class AfterLoads>
 __device__ __forceinline__ void qpack_block(QpackShared<L>& sh, QpackOut<L>& o, const uint16_t* __restrict__ qg,
-                                            const float* __restrict__ Pbh, int G) {
+                                            const float* __restrict__ Pbh, int G, AfterLoads&& after_loads) {
   static_assert((L * 32) % NT == 0 && 4 * L <= NT, "thread count");
   constexpr int PV = L * 32 / NT;  // 16-byte units of P per thread
   const int t = threadIdx.x, lane = t & 63, wid = t >> 6;
@@ -144,6 +146,7 @@ __device__ __forceinline__ void qpack_block(QpackShared<L>& sh, QpackOut<L>& o, 
     for (int r = 0; r < PV; ++r) pv[r] = reinterpret_cast<const float4*>(Pbh)[t + NT * r];
     uint4 qv = make_uint4(0u, 0u, 0u, 0u);
     if (t < G * (kHeadDim / 8)) qv = reinterpret_cast<const uint4*>(qg)[t];
+    after_loads();
 #pragma unroll
     for (int r = 0; r < PV; ++r) {
       const int f = t + NT * r;  // unit f of P: row f / 32, block (f / 8) mod 4, unit f mod 8
@@ -327,11 +330,15 @@ __device__ __forceinline__ void score_body(ScoreShared<L>& sh, int bh, int s, co
       return load_code_group<W>(cb, n, cnt, vec_ok);
   };
 
-  // the query planes of (b, h), packed before any code load is issued; they
-  // are uniform (scalar registers).  Slice 0 also stores them (and sum |p|)
-  // for the attention kernel and the caller.
+  // the query planes of (b, h); they are uniform (scalar registers).  Slice
+  // 0 also stores them (and sum |p|) for the attention kernel and the
+  // caller.  The first code load of the ring is issued behind the P loads
+  // and lands while the query is packed; the other RD - 1 follow the packing
+  // (more loads in flight during it delay P for the workgroups dispatched
+  // later on the CU, and the step gets slower).
+  u32x4_t cw[RD];
   qpack_block<L, NT>(sh.u.qp, sh.qo, q + ((size_t)b * Hkv * G + (size_t)h * G) * kHeadDim, P + b * sP_b + h * sP_h,
-                     G);
+                     G, [&]() { cw[0] = load_group(0); });
   BPC_STAMP(1, 5);
   const uint32_t* qcw = reinterpret_cast<const uint32_t*>(sh.qo.qc16);
   uint32_t sg[W], M[7][W];
@@ -347,9 +354,8 @@ __device__ __forceinline__ void score_body(ScoreShared<L>& sh, int bh, int s, co
   }
   // a ring of RD code loads per thread stays in flight: the load of group
   // it + RD is issued as soon as group it has been consumed
-  u32x4_t cw[RD];
 #pragma unroll
-  for (int r = 0; r < RD; ++r) cw[r] = load_group(r);
+  for (int r = 1; r < RD; ++r) cw[r] = load_group(r);
   if (s == 0 && threadIdx.x <= 8 * W) {
     const uint32_t v = threadIdx.x < 8 * W ? qcw[threadIdx.x] : (uint32_t)T;
     qcode_ws[(size_t)bh * kQcodeStride + threadIdx.x] = v;
