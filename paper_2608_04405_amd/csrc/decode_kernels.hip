@@ -281,8 +281,8 @@ struct ScoreShared {
   QpackOut<L> qo;
   uint32_t coarse[kCoarseBins];
   uint32_t cc[kCoarseBins + 1];
-  int cnt[128];
-  int cs, kth, cmin, total, cs2, that;
+  int cnt[kScoreThreads / 64];  // candidates per wavefront
+  int kth, cmin, that;
 };
 
 // FULL: the slice holds kSlice keys and its codes are 16-byte aligned, so no
@@ -459,24 +459,26 @@ __device__ __forceinline__ void score_body(ScoreShared<L>& sh, int bh, int s, co
     const int cs2 = min(h0 < 64 ? 2 * h0 : 1 << 30, h1 < 64 ? 2 * h1 + 1 : 1 << 30);
     const unsigned long long z0 = __ballot(c0 != 0u), z1 = __ballot(c1 != 0u);
     const int g0 = first_lane(z0), g1 = first_lane(z1);
+    // the first fine bin of coarse bin c where the count reaches `need`
+    // (NB - 1 when c < 0, i.e. the slice holds fewer than k keys): lane l
+    // tests bins l and l + 64 of c, whose prefix form adds the count below c
+    static_assert(kCoarseShift == 7, "two fine bins of a coarse bin per lane");
+    auto fine_first = [&](int c, int need) -> int {
+      if (c < 0 || c >= kCoarseBins) return NB - 1;
+      const int below = __builtin_amdgcn_readlane((c & 1) ? ex + (int)c0 : ex, c >> 1);
+      const int t0 = (c << kCoarseShift) + lane, t1 = t0 + 64;
+      const uint32_t v0 = (t0 < NBP) ? sh.u.hist[t0] : 0u, v1 = (t1 < NBP) ? sh.u.hist[t1] : 0u;
+      const unsigned long long r0 = __ballot(below + (int)(v0 >> 16) + (int)(v0 & 0xFFFFu) >= need);
+      const unsigned long long r1 = __ballot(below + (int)(v1 >> 16) + (int)(v1 & 0xFFFFu) >= need);
+      return r0 ? (c << kCoarseShift) + first_lane(r0) : r1 ? (c << kCoarseShift) + 64 + first_lane(r1) : NB - 1;
+    };
+    const int kth_w = fine_first((cnt >= k) ? cs : -1, k);
+    const int that_w = fine_first(cs2, mloc);  // mloc <= cnt: always found
     if (lane == 0) {
-      sh.cs = (cnt >= k) ? cs : -1;
-      sh.cs2 = cs2;  // mloc <= cnt: always found
-      sh.kth = NB - 1;
-      sh.that = NB - 1;
+      sh.kth = kth_w;
+      sh.that = that_w;
       sh.cmin = min(g0 < 64 ? 2 * g0 : kCoarseBins - 1, g1 < 64 ? 2 * g1 + 1 : kCoarseBins - 1);
     }
-  }
-  __syncthreads();
-  if (threadIdx.x < 2 << kCoarseShift) {
-    // the first fine bin of coarse bin cs (threads 0..127) where the count
-    // reaches k, and of cs2 (threads 128..255) where it reaches mloc
-    const bool second = threadIdx.x >= (1 << kCoarseShift);
-    const int cs = second ? sh.cs2 : sh.cs, need = second ? mloc : k;
-    const int t = (max(cs, 0) << kCoarseShift) + (threadIdx.x & ((1 << kCoarseShift) - 1));
-    const uint32_t v = (t < NBP) ? sh.u.hist[t] : 0u;
-    const unsigned long long m = __ballot(cs >= 0 && (int)sh.cc[max(cs, 0)] + (int)(v >> 16) + (int)(v & 0xFFFFu) >= need);
-    if (m && lane == first_lane(m)) atomicMin(second ? &sh.that : &sh.kth, t);
   }
   __syncthreads();
   const int kth = sh.kth;
@@ -543,16 +545,14 @@ __device__ __forceinline__ void score_body(ScoreShared<L>& sh, int bh, int s, co
 #pragma unroll
   for (int i = 0; i < PER / 2; ++i) __asm__ volatile("" : "+v"(dpk[i]));
   __syncthreads();
-  if (threadIdx.x < 64) {
+  int total;  // the slice's candidate count
+  {
+    // every wavefront scans the NW counts itself: its own offset and the total
     const int v = (lane < NW) ? sh.cnt[lane] : 0;
     const int x = wave_inclusive_sum(v);
-    if (lane < NW) sh.cnt[64 + lane] = x - v;
-    if (lane == 63) sh.total = x;
-  }
-  __syncthreads();
-  {
+    total = __builtin_amdgcn_readlane(x, 63);
     uint32_t* cs_out = cand + sl * kSlice;
-    int base = sh.cnt[64 + wid];  // uniform over the wavefront
+    int base = __builtin_amdgcn_readlane(x - v, wid);  // uniform over the wavefront
 #pragma unroll
     for (int it = 0; it < NLD; ++it) {
       int pos = base;
@@ -569,7 +569,7 @@ __device__ __forceinline__ void score_body(ScoreShared<L>& sh, int bh, int s, co
         if (f[u]) cs_out[pos++] = ((uint32_t)key_of(it, u) << 16) | (uint32_t)dist_of(it, u);
     }
   }
-  if (threadIdx.x == 0) *reinterpret_cast<uint4*>(meta + sl * 4) = make_uint4(kth, cmin, sh.total, cand_max);
+  if (threadIdx.x == 0) *reinterpret_cast<uint4*>(meta + sl * 4) = make_uint4(kth, cmin, total, cand_max);
   if (score_out) {  // debug output
     int32_t* so = score_out + (size_t)bh * N + n0;
 #pragma unroll
