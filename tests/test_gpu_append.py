@@ -15,6 +15,7 @@ import pytest
 import torch
 
 import oracle
+from _helpers import oracle_build_of
 from workloads import CONFIGS, make_layer
 
 pytestmark = pytest.mark.gpu
@@ -99,7 +100,13 @@ def test_decode_loop_with_append():
     codes = torch.zeros(cfg.B, cfg.Hkv, Ncap, cfg.W, dtype=torch.int32, device=DEV)
     P, _, _ = bpc.build_hash(K, d["G"].to(DEV), N=cfg.N, codes_out=codes)
     torch.cuda.synchronize()
-    Pn = P.cpu().numpy()
+    # the oracle side keeps its own cache: its build of the prefill keys,
+    # then the appended rows and the codes its Algorithm 2 gives them
+    Pn, cref, _ = oracle_build_of(P, codes, K, d["G"], [(0, h) for h in range(cfg.Hkv)], N=cfg.N)
+    cref[:, :, cfg.N:] = 0
+    Kref = np.zeros((cfg.B, cfg.Hkv, Ncap, 128), np.uint16)
+    Vref = np.zeros_like(Kref)
+    Kref[:, :, :cfg.N], Vref[:, :, :cfg.N] = bits(d["K"]), bits(d["V"])
     sm = 1.0 / math.sqrt(128)
     q_next = randn_bf16(rng, (cfg.B, cfg.Hq, 128))
     for t in range(steps):
@@ -116,12 +123,14 @@ def test_decode_loop_with_append():
         idx = torch.empty(cfg.B, cfg.Hkv, k, dtype=torch.int32, device=DEV)
         out = bpc.decode_attention(q, K, V, codes, P, k, sm, N=N, idx_out=idx)
         torch.cuda.synchronize()
-        Kb, Vb, cn = bits(K), bits(V), u32(codes)
+        cn = u32(codes)
+        Kref[:, :, N - 1], Vref[:, :, N - 1] = bits(kn)[:, :, 0], bits(vn)[:, :, 0]
         for h in range(cfg.Hkv):
             new_codes, _, _ = oracle.hash_keys(bits(kn)[0, h], Pn[0, h])
             assert np.array_equal(cn[0, h, N - 1:N], new_codes), f"step {t}: appended code differs at head {h}"
-            ref = oracle.decode_head(bits(q)[0, h * cfg.G:(h + 1) * cfg.G], Kb[0, h, :N], Vb[0, h, :N], cn[0, h, :N],
-                                     Pn[0, h], k, sm)
+            cref[0, h, N - 1:N] = new_codes
+            ref = oracle.decode_head(bits(q)[0, h * cfg.G:(h + 1) * cfg.G], Kref[0, h, :N], Vref[0, h, :N],
+                                     cref[0, h, :N], Pn[0, h], k, sm)
             assert np.array_equal(idx[0, h].cpu().numpy(), ref["idx"]), f"step {t}: indices differ at head {h}"
             e = rel_err(out[0, h * cfg.G:(h + 1) * cfg.G].cpu().numpy(), ref["out"])
             assert np.all(e <= TOL), f"step {t}: output error {e.max():.3g} at head {h}"

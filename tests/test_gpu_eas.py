@@ -17,6 +17,7 @@ import pytest
 import torch
 
 import oracle
+from _helpers import oracle_build_of
 from workloads import CONFIGS, make_layer
 
 pytestmark = pytest.mark.gpu
@@ -75,24 +76,26 @@ def test_select_hard_parity(B, H, N, m, pool):
 
 
 def test_select_hard_strided_from_build():
+    """The reconstruction errors of a real build (the oracle's Algorithm 1
+    on the tiny workload, rounded to float32 as the prefill kernels store
+    them) in a buffer with a row stride past N."""
     cfg = CONFIGS[0]
-    d = make_layer(cfg, device=DEV)
+    d = make_layer(cfg, device="cpu")
+    Kb, Gn = bits(d["K"]), d["G"].numpy()
+    eo = np.stack([oracle.build_binary_pcs(Kb[0, h], Gn)[2] for h in range(cfg.Hkv)]).astype(np.float32)
     Ncap = cfg.N + 40
     err = torch.full((cfg.B, cfg.Hkv, Ncap), -7.0, device=DEV)  # the tail past N must be ignored
-    bpc.build_hash(d["K"], d["G"].to(DEV), err_out=err[:, :, :cfg.N].contiguous())
-    P, codes, e2 = bpc.build_hash(d["K"], d["G"].to(DEV), err_out=torch.empty(cfg.B, cfg.Hkv, cfg.N, device=DEV))
-    err[:, :, :cfg.N] = e2
+    err[0, :, :cfg.N] = torch.from_numpy(eo).to(DEV)
     _, m = oracle.eas_budget(cfg.k)
     serr = bpc.select_hard(err, m, N=cfg.N)
     torch.cuda.synchronize()
-    en = err.cpu().numpy()
     for h in range(cfg.Hkv):
-        assert np.array_equal(serr[0, h].cpu().numpy(), oracle.select_hard(en[0, h, :cfg.N], m))
+        assert np.array_equal(serr[0, h].cpu().numpy(), oracle.select_hard(eo[h], m))
 
 
 # ------------------------------------------------------------------ decode with the safeguard
 
-def _eas_compare(q, K, V, codes_np, P_np, k, serr_np, N=None, label=""):
+def _eas_compare(q, K, V, codes_np, P_np, k, serr_np, N=None, label="", heads=None):
     B, Hq, D = q.shape
     Hkv = K.shape[1]
     Gq = Hq // Hkv
@@ -108,17 +111,36 @@ def _eas_compare(q, K, V, codes_np, P_np, k, serr_np, N=None, label=""):
     torch.cuda.synchronize()
     qb, Kb, Vb = bits(q), bits(K), bits(V)
     worst = 0.0
-    for b in range(B):
-        for h in range(Hkv):
-            ref = oracle.decode_head_eas(qb[b, h * Gq:(h + 1) * Gq], Kb[b, h, :N], Vb[b, h, :N], codes_np[b, h, :N],
-                                         P_np[b, h], k, serr_np[b, h], sm)
-            assert np.array_equal(idx[b, h].cpu().numpy(), ref["idx"]), f"{label}: S_hash differs at {(b, h)}"
-            assert np.array_equal(added[b, h].cpu().numpy(), ref["added"]), f"{label}: added flags differ at {(b, h)}"
-            e = rel_err(out[b, h * Gq:(h + 1) * Gq].cpu().numpy(), ref["out"])
-            worst = max(worst, float(e.max()))
-            assert np.all(e <= TOL), f"{label}: output error {e.max():.3g} at {(b, h)}"
+    for b, h in (heads or [(b, h) for b in range(B) for h in range(Hkv)]):
+        ref = oracle.decode_head_eas(qb[b, h * Gq:(h + 1) * Gq], Kb[b, h, :N], Vb[b, h, :N], codes_np[b, h, :N],
+                                     P_np[b, h], k, serr_np[b, h], sm)
+        assert np.array_equal(idx[b, h].cpu().numpy(), ref["idx"]), f"{label}: S_hash differs at {(b, h)}"
+        assert np.array_equal(added[b, h].cpu().numpy(), ref["added"]), f"{label}: added flags differ at {(b, h)}"
+        e = rel_err(out[b, h * Gq:(h + 1) * Gq].cpu().numpy(), ref["out"])
+        worst = max(worst, float(e.max()))
+        assert np.all(e <= TOL), f"{label}: output error {e.max():.3g} at {(b, h)}"
     announce(f"{label}: max relative output error {worst:.3g}")
     return out
+
+
+def _gpu_pipeline_vs_oracle(cfg, heads, label):
+    """GPU: Algorithm 1, select_hard on its float32 errors, decode over
+    S_hash u S_err.  Oracle: its own build of the checked heads, its
+    selection from its own errors (rounded to float32 as the kernels store
+    them), its decode.  The GPU's P, codes and hard sets are checked equal
+    to the oracle's first; the checked heads then hold the oracle's values."""
+    d = make_layer(cfg, device=DEV)
+    P, codes, err = bpc.build_hash(d["K"], d["G"].to(DEV), err_out=torch.empty(cfg.B, cfg.Hkv, cfg.N, device=DEV))
+    k_hash, m = oracle.eas_budget(cfg.k)
+    serr = bpc.select_hard(err, m)
+    torch.cuda.synchronize()
+    Pn, cn, errs = oracle_build_of(P, codes, d["K"], d["G"], heads)
+    sn = serr.cpu().numpy().astype(np.int64)
+    for (b, h), eo in errs.items():
+        so = oracle.select_hard(eo.astype(np.float32), m)
+        assert np.array_equal(sn[b, h], so), f"{label}: hard set differs at {(b, h)}"
+        sn[b, h] = so
+    _eas_compare(d["q"], d["K"], d["V"], cn, Pn, k_hash, sn, label=label, heads=heads)
 
 
 def test_decode_eas_tiny_budget_split():
@@ -126,23 +148,13 @@ def test_decode_eas_tiny_budget_split():
     hard set, chosen on the GPU from the GPU build's errors."""
     cfg = CONFIGS[0]
     announce(f"[eas tiny] {cfg}")
-    d = make_layer(cfg, device=DEV)
-    P, codes, err = bpc.build_hash(d["K"], d["G"].to(DEV), err_out=torch.empty(cfg.B, cfg.Hkv, cfg.N, device=DEV))
-    k_hash, m = oracle.eas_budget(cfg.k)
-    serr = bpc.select_hard(err, m)
-    torch.cuda.synchronize()
-    _eas_compare(d["q"], d["K"], d["V"], u32(codes), P.cpu().numpy(), k_hash, serr.cpu().numpy(), label="eas tiny")
+    _gpu_pipeline_vs_oracle(cfg, [(0, h) for h in range(cfg.Hkv)], "eas tiny")
 
 
 def test_decode_eas_llama8b_shape():
     cfg = CONFIGS[1]
     announce(f"[eas llama8b] {cfg}")
-    d = make_layer(cfg, device=DEV)
-    P, codes, err = bpc.build_hash(d["K"], d["G"].to(DEV), err_out=torch.empty(cfg.B, cfg.Hkv, cfg.N, device=DEV))
-    k_hash, m = oracle.eas_budget(cfg.k)
-    serr = bpc.select_hard(err, m)
-    torch.cuda.synchronize()
-    _eas_compare(d["q"], d["K"], d["V"], u32(codes), P.cpu().numpy(), k_hash, serr.cpu().numpy(), label="eas llama8b")
+    _gpu_pipeline_vs_oracle(cfg, [(0, 0), (0, 5)], "eas llama8b")
 
 
 def _random_case(rng, B, Hq, Hkv, N, L):

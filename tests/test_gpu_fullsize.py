@@ -132,8 +132,9 @@ def build_decode_case(name, sample, hash_rows, eas=False, budgets=(), per_head=F
     compare_sampled_head(d, P_ref, codes_ref, b, h, cfg, out, idx, sc, qc, f"{name} head {(b, h)}")
     if eas:
         # the safeguard at full size: 10 % of the budget for the hard set,
-        # chosen on the GPU from the GPU build's errors (the same float32
-        # errors go to the oracle's selection)
+        # chosen on the GPU from the GPU build's errors; the oracle selects
+        # from its own build's errors, rounded to float32 as the kernels
+        # store them
         k_hash, m = oracle.eas_budget(cfg.k)
         serr = bpc.select_hard(err, m)
         idx2 = torch.empty(cfg.B, cfg.Hkv, k_hash, dtype=torch.int32, device=DEV)
@@ -141,11 +142,11 @@ def build_decode_case(name, sample, hash_rows, eas=False, budgets=(), per_head=F
         out2 = bpc.decode_attention(d["q"], d["K"], d["V"], codes, P, k_hash, N=cfg.N, idx_out=idx2, serr=serr,
                                     added_out=added)
         torch.cuda.synchronize()
-        serr_n = serr[b, h].cpu().numpy()
-        assert np.array_equal(serr_n, oracle.select_hard(err[b, h].cpu().numpy(), m)), f"{name}: hard set differs"
+        serr_ref = oracle.select_hard(err_ref.astype(np.float32), m)
+        assert np.array_equal(serr[b, h].cpu().numpy(), serr_ref), f"{name}: hard set differs"
         sm = 1.0 / np.sqrt(cfg.D)
         ref = oracle.decode_head_eas(bits(d["q"][b, h * cfg.G:(h + 1) * cfg.G]), Kb, bits(d["V"][b, h, :cfg.N]),
-                                     codes_ref, P_ref, k_hash, serr_n, sm)
+                                     codes_ref, P_ref, k_hash, serr_ref, sm)
         assert np.array_equal(idx2[b, h].cpu().numpy(), ref["idx"]), f"{name}: safeguard S_hash differs"
         assert np.array_equal(added[b, h].cpu().numpy(), ref["added"]), f"{name}: safeguard flags differ"
         e = rel_err(out2[b, h * cfg.G:(h + 1) * cfg.G].cpu().numpy(), ref["out"])

@@ -16,6 +16,7 @@ import pytest
 import torch
 
 import oracle
+from _helpers import oracle_build_of
 from workloads import CONFIGS, make_layer
 
 pytestmark = pytest.mark.gpu
@@ -46,7 +47,7 @@ def announce(msg):
     print(msg, flush=True)
 
 
-def compare(q, K, V, codes, P, k, N, label, P_np=None, heads=None):
+def compare(q, K, V, codes, P, k, N, label, P_np=None, heads=None, codes_np=None):
     B, Hq, D = q.shape
     Hkv = K.shape[1]
     G = Hq // Hkv
@@ -58,7 +59,8 @@ def compare(q, K, V, codes, P, k, N, label, P_np=None, heads=None):
     out = bpc.decode_attention_per_head(q, K, V, codes, P, k, sm, N=N, idx_out=idx, score_out=sc, qcode_out=qc)
     torch.cuda.synchronize()
     P_np = P.cpu().numpy() if P_np is None else P_np
-    qb, Kb, Vb, cn = bits(q), bits(K), bits(V), u32(codes)
+    qb, Kb, Vb = bits(q), bits(K), bits(V)
+    cn = u32(codes) if codes_np is None else codes_np
     worst = 0.0
     for b, h in (heads or [(b, h) for b in range(B) for h in range(Hkv)]):
         Ph = P_np[b, h] if P_np.ndim == 4 else P_np[h]
@@ -80,7 +82,8 @@ def test_per_head_group_of_one_is_the_decode_step():
     announce(f"[per head] {cfg}")
     d = make_layer(cfg, device=DEV)
     P, codes, _ = bpc.build_hash(d["K"], d["G"].to(DEV))
-    out, idx = compare(d["q"], d["K"], d["V"], codes, P, cfg.k, cfg.N, "per head G=1")
+    Pn, cn, _ = oracle_build_of(P, codes, d["K"], d["G"], [(0, h) for h in range(cfg.Hkv)])
+    out, idx = compare(d["q"], d["K"], d["V"], codes, P, cfg.k, cfg.N, "per head G=1", P_np=Pn, codes_np=cn)
     idx_g = torch.empty(cfg.B, cfg.Hkv, cfg.k, dtype=torch.int32, device=DEV)
     out_g = bpc.decode_attention(d["q"], d["K"], d["V"], codes, P, cfg.k, idx_out=idx_g)
     torch.cuda.synchronize()
@@ -92,7 +95,10 @@ def test_per_head_llama8b_ragged():
     announce(f"[per head] {cfg}")
     d = make_layer(cfg, device=DEV)
     P, codes, _ = bpc.build_hash(d["K"], d["G"].to(DEV))
-    _, idx = compare(d["q"], d["K"], d["V"], codes, P, cfg.k, cfg.N, "per head 8B-shaped")
+    heads = [(0, 0), (1, 5)]
+    Pn, cn, _ = oracle_build_of(P, codes, d["K"], d["G"], heads)
+    _, idx = compare(d["q"], d["K"], d["V"], codes, P, cfg.k, cfg.N, "per head 8B-shaped", P_np=Pn, heads=heads,
+                     codes_np=cn)
     # the heads of a group do select differently (else the variant were moot)
     idn = idx.cpu().numpy()
     assert any(not np.array_equal(idn[0, 0], idn[0, g]) for g in range(1, cfg.G))
@@ -120,4 +126,5 @@ def test_per_head_group_of_eight():
     q = torch.from_numpy(rng.standard_normal((B, Hkv * G, 128)).astype(np.float32)).to(torch.bfloat16).to(DEV)
     G_dirs = torch.from_numpy(rng.standard_normal((L, 128)).astype(np.float32)).to(DEV)
     P, codes, _ = bpc.build_hash(K, G_dirs)
-    compare(q, K, V, codes, P, k, N, "per head G=8")
+    Pn, cn, _ = oracle_build_of(P, codes, K, G_dirs, [(0, 0)])
+    compare(q, K, V, codes, P, k, N, "per head G=8", P_np=Pn, codes_np=cn)
