@@ -115,37 +115,93 @@ def _stream(stream) -> Optional[int]:
 
 
 def _need(t: torch.Tensor, name: str, dtype, dim: int) -> None:
+    """dtype, number of dims and a contiguous innermost dimension; the device
+    is checked separately (`_on_gpu`), after every shape check, so that a
+    shape mistake is reported as such wherever the tensors live."""
     if not isinstance(t, torch.Tensor):
         raise TypeError(f"{name} must be a torch.Tensor")
     if t.dtype != dtype:
         raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
-    if t.device.type != "cuda":
-        raise ValueError(f"{name} must be on a GPU")
     if t.dim() != dim:
         raise ValueError(f"{name} must have {dim} dims, got shape {tuple(t.shape)}")
-    if t.stride(-1) != 1:
+    if t.numel() and t.stride(-1) != 1:
         raise ValueError(f"{name}: innermost dimension must be contiguous")
+
+
+def _extent(t: torch.Tensor, name: str, spec) -> None:
+    """Check every extent of t against spec: an int is an exact size, ("ge",
+    n) a lower bound (a cache with room for more rows), None anything."""
+    shape = tuple(t.shape)
+    if len(shape) != len(spec):
+        raise ValueError(f"{name} must have {len(spec)} dims, got shape {shape}")
+    for i, (got, want) in enumerate(zip(shape, spec)):
+        if want is None:
+            continue
+        if isinstance(want, tuple):
+            if got < want[1]:
+                raise ValueError(f"{name}: dim {i} is {got}, needs at least {want[1]} (shape {shape})")
+        elif got != want:
+            raise ValueError(f"{name}: dim {i} is {got}, expected {want} (shape {shape})")
+
+
+def _exact_out(t: Optional[torch.Tensor], name: str, dtype, shape) -> None:
+    """An optional output the kernels address as a dense array of `shape`."""
+    if t is None:
+        return
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if tuple(t.shape) != tuple(shape) or not t.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous tensor of shape {tuple(shape)}, got {tuple(t.shape)}")
+
+
+def _on_gpu(*tensors) -> None:
+    """Every given tensor (None entries skipped) on one GPU."""
+    dev = None
+    for t in tensors:
+        if t is None:
+            continue
+        if t.device.type != "cuda":
+            raise ValueError("every tensor must be on a GPU")
+        if dev is None:
+            dev = t.device
+        elif t.device != dev:
+            raise ValueError(f"tensors on different devices: {dev} and {t.device}")
+
+
+def _budget(k: int, N: int, Ncap: int) -> None:
+    if not 1 <= N <= Ncap:
+        raise ValueError(f"N={N} must satisfy 1 <= N <= {Ncap} (the rows the cache holds)")
+    if not 1 <= k <= N:
+        raise ValueError(f"k={k} must satisfy 1 <= k <= N={N}")
 
 
 def _kv_strides(t: torch.Tensor):
     return t.stride(0), t.stride(1), t.stride(2)
 
 
-def _proj(P: torch.Tensor, D: int = 128):
+def _proj(P: torch.Tensor, D: int = 128, B: Optional[int] = None, Hkv: Optional[int] = None):
     """(L, sP_b, sP_h) of a projection given as [B, Hkv, L, D] (one per
     (sequence, KV head)), [Hkv, L, D] (one per KV head, shared by the batch:
-    offline calibration) or [L, D] (one for everything)."""
-    if P.dtype != torch.float32 or P.device.type != "cuda":
-        raise TypeError("P must be a float32 GPU tensor")
-    if P.stride(-1) != 1 or P.shape[-1] != D or (P.dim() >= 2 and P.shape[-2] > 1 and P.stride(-2) != D):
+    offline calibration) or [L, D] (one for everything).  When B and Hkv are
+    given, the leading dims must match them."""
+    if not isinstance(P, torch.Tensor) or P.dtype != torch.float32:
+        raise TypeError("P must be a float32 tensor")
+    if P.dim() not in (2, 3, 4):
+        raise ValueError("P must be [B, Hkv, L, 128], [Hkv, L, 128] or [L, 128]")
+    if P.stride(-1) != 1 or P.shape[-1] != D or (P.shape[-2] > 1 and P.stride(-2) != D):
         raise ValueError("P rows must be contiguous [.., L, 128]")
+    L = P.shape[-2]
+    if L not in (32, 64, 128):
+        raise ValueError(f"P has {L} rows: the code length must be 32, 64 or 128")
+    if P.dim() == 3 and Hkv is not None and P.shape[0] != Hkv:
+        raise ValueError(f"P is [Hkv, L, 128] with {P.shape[0]} heads, expected Hkv={Hkv}")
+    if P.dim() == 4 and B is not None and (P.shape[0], P.shape[1]) != (B, Hkv):
+        raise ValueError(f"P is {tuple(P.shape)}, expected [{B}, {Hkv}, L, 128]")
     if P.dim() == 2:
-        return P.shape[0], 0, 0
+        return L, 0, 0
     if P.dim() == 3:
-        return P.shape[1], 0, P.stride(0)
-    if P.dim() == 4:
-        return P.shape[2], P.stride(0), P.stride(1)
-    raise ValueError("P must be [B, Hkv, L, 128], [Hkv, L, 128] or [L, 128]")
+        return L, 0, P.stride(0)
+    return L, P.stride(0), P.stride(1)
 
 
 def build_workspace_bytes(B: int, Hkv: int, N: int, L: int, D: int = 128) -> int:
@@ -163,9 +219,16 @@ def decode_per_head_workspace_bytes(B: int, Hq: int, Hkv: int, N: int, L: int, k
 def _u32_codes(codes: torch.Tensor, name: str = "codes") -> torch.Tensor:
     # torch has no uint32 arithmetic on every build; int32 storage is used and
     # reinterpreted by the library.
-    if codes.dtype not in (torch.int32, torch.uint32):
+    if not isinstance(codes, torch.Tensor) or codes.dtype not in (torch.int32, torch.uint32):
         raise TypeError(f"{name} must be int32/uint32 storage")
+    if codes.dim() != 4 or (codes.numel() and codes.stride(-1) != 1) or (codes.shape[2] > 1 and codes.stride(2) != codes.shape[3]):
+        raise ValueError(f"{name} must be [B, Hkv, Ncap, L/32] with the words of a key and the keys of a head contiguous")
     return codes
+
+
+def _fragile(fragile: Optional[torch.Tensor]) -> None:
+    if fragile is not None and (fragile.dtype != torch.int64 or fragile.numel() < 1):
+        raise ValueError("fragile must be an int64 tensor with at least one element")
 
 
 def build_hash(K: torch.Tensor, G: torch.Tensor, N: Optional[int] = None, *,
@@ -175,21 +238,35 @@ def build_hash(K: torch.Tensor, G: torch.Tensor, N: Optional[int] = None, *,
     """Binary principal components of every (b, h): returns (P, codes, err).
 
     K [B, Hkv, >=N, 128] bf16; G [L, 128] fp32 Gaussian directions.  codes
-    are int32 storage [B, Hkv, Ncap, L/32] holding the packed bits.  When
-    `fragile` (a 1-element int64 GPU tensor) is given, the number of fragile
-    sign decisions is added to it."""
+    are int32 storage [B, Hkv, Ncap, L/32] holding the packed bits; err_out,
+    when given, is a contiguous [B, Hkv, N] fp32 tensor.  When `fragile` (a
+    1-element int64 GPU tensor) is given, the number of fragile sign
+    decisions is added to it."""
     _need(K, "K", torch.bfloat16, 4)
     B, Hkv, Ncap, D = K.shape
     N = Ncap if N is None else N
+    if not 1 <= N <= Ncap:
+        raise ValueError(f"N={N} must satisfy 1 <= N <= {Ncap}")
     _need(G, "G", torch.float32, 2)
-    G = G.contiguous()
     L = G.shape[0]
+    _extent(G, "G", (L, D))
+    if L not in (32, 64, 128):
+        raise ValueError(f"G has {L} rows: the code length must be 32, 64 or 128")
+    G = G.contiguous()
+    W = L // 32
+    if P_out is not None:
+        _exact_out(P_out, "P_out", torch.float32, (B, Hkv, L, D))
+    if codes_out is not None:
+        _u32_codes(codes_out, "codes_out")
+        _extent(codes_out, "codes_out", (B, Hkv, ("ge", N), W))
+    _exact_out(err_out, "err_out", torch.float32, (B, Hkv, N))
+    _fragile(fragile)
+    _on_gpu(K, G, P_out, codes_out, err_out, fragile, workspace)
     dev = K.device
     if P_out is None:
         P_out = torch.empty(B, Hkv, L, D, dtype=torch.float32, device=dev)
     if codes_out is None:
-        codes_out = torch.zeros(B, Hkv, Ncap, max(1, L // 32), dtype=torch.int32, device=dev)
-    _u32_codes(codes_out, "codes_out")
+        codes_out = torch.zeros(B, Hkv, Ncap, W, dtype=torch.int32, device=dev)
     ws_bytes = build_workspace_bytes(B, Hkv, N, L, D)
     if workspace is None:
         workspace = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
@@ -205,19 +282,48 @@ def hash_keys(K: torch.Tensor, P: torch.Tensor, N: Optional[int] = None, *,
               fragile: Optional[torch.Tensor] = None, stream=None):
     """Hash keys against P (Algorithm 2).  P is [B, Hkv, L, 128], or
     [Hkv, L, 128] / [L, 128] shared across the batch (offline calibration).
-    Returns (codes, err)."""
+    err_out, when given, is a contiguous [B, Hkv, N] fp32 tensor.  Returns
+    (codes, err)."""
     _need(K, "K", torch.bfloat16, 4)
     B, Hkv, Ncap, D = K.shape
     N = Ncap if N is None else N
-    L, sPb, sPh = _proj(P, D)
+    if not 1 <= N <= Ncap:
+        raise ValueError(f"N={N} must satisfy 1 <= N <= {Ncap}")
+    L, sPb, sPh = _proj(P, D, B, Hkv)
+    if codes_out is not None:
+        _u32_codes(codes_out, "codes_out")
+        _extent(codes_out, "codes_out", (B, Hkv, ("ge", N), L // 32))
+    _exact_out(err_out, "err_out", torch.float32, (B, Hkv, N))
+    _fragile(fragile)
+    _on_gpu(K, P, codes_out, err_out, fragile)
     if codes_out is None:
-        codes_out = torch.zeros(B, Hkv, Ncap, max(1, L // 32), dtype=torch.int32, device=K.device)
-    _u32_codes(codes_out, "codes_out")
+        codes_out = torch.zeros(B, Hkv, Ncap, L // 32, dtype=torch.int32, device=K.device)
     _check(_lib.bpc_hash_keys(_ptr(K), *_kv_strides(K), B, Hkv, N, D, L, _ptr(P), sPb, sPh, _ptr(codes_out),
                               codes_out.stride(0), codes_out.stride(1), _ptr(err_out), _ptr(fragile),
                               _stream(stream)),
            "bpc_hash_keys")
     return codes_out, err_out
+
+
+def _decode_inputs(q, K, V, codes, P, k, N):
+    """Shape checks shared by the decode entry points; returns the sizes."""
+    _need(q, "q", torch.bfloat16, 3)
+    _need(K, "K", torch.bfloat16, 4)
+    _need(V, "V", torch.bfloat16, 4)
+    if not q.is_contiguous():
+        raise ValueError("q must be contiguous")
+    B, Hq, D = q.shape
+    _, Hkv, Ncap, _ = K.shape
+    N = Ncap if N is None else N
+    _extent(K, "K", (B, Hkv, ("ge", 1), D))
+    _budget(k, N, Ncap)
+    _extent(V, "V", (B, Hkv, ("ge", N), D))
+    if Hq % Hkv:
+        raise ValueError(f"Hq={Hq} must be a multiple of Hkv={Hkv}")
+    L, sPb, sPh = _proj(P, D, B, Hkv)
+    _u32_codes(codes)
+    _extent(codes, "codes", (B, Hkv, ("ge", N), L // 32))
+    return B, Hq, Hkv, D, N, L, sPb, sPh
 
 
 def decode_attention(q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, codes: torch.Tensor,
@@ -231,7 +337,8 @@ def decode_attention(q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, codes: t
 
     q [B, Hq, 128] bf16 contiguous; K, V [B, Hkv, >=N, 128] bf16; codes
     int32 storage [B, Hkv, >=N, L/32]; P [B, Hkv, L, 128] fp32, or shared
-    across the batch as [Hkv, L, 128] (offline calibration) or [L, 128].  Optional debug outputs: idx_out [B, Hkv, k] int32,
+    across the batch as [Hkv, L, 128] (offline calibration) or [L, 128].
+    Optional debug outputs (contiguous): idx_out [B, Hkv, k] int32,
     score_out [B, Hkv, N] int32, qcode_out [B, Hkv, 8, L/32] int32.
     `events`: BPC_DECODE_STAGES + 1 torch.cuda.Event objects recorded at the
     stage boundaries (for measurement).
@@ -240,16 +347,28 @@ def decode_attention(q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, codes: t
     attention runs over the union of the k hash-selected keys and serr (the
     error-aware safeguard); added_out [B, Hkv, m] int32 then marks the
     entries of serr that the hash selection had not taken."""
-    _need(q, "q", torch.bfloat16, 3)
-    _need(K, "K", torch.bfloat16, 4)
-    _need(V, "V", torch.bfloat16, 4)
-    if not q.is_contiguous():
-        raise ValueError("q must be contiguous")
-    B, Hq, D = q.shape
-    _, Hkv, Ncap, _ = K.shape
-    N = Ncap if N is None else N
-    _u32_codes(codes)
-    L, sPb, sPh = _proj(P, D)
+    B, Hq, Hkv, D, N, L, sPb, sPh = _decode_inputs(q, K, V, codes, P, k, N)
+    _exact_out(out, "out", torch.float32, (B, Hq, D))
+    _exact_out(idx_out, "idx_out", torch.int32, (B, Hkv, k))
+    _exact_out(score_out, "score_out", torch.int32, (B, Hkv, N))
+    _exact_out(qcode_out, "qcode_out", torch.int32, (B, Hkv, 8, L // 32))
+    m = 0
+    if serr is not None:
+        if events is not None or score_out is not None or qcode_out is not None:
+            raise ValueError("serr cannot be combined with events, score_out or qcode_out")
+        if not isinstance(serr, torch.Tensor) or serr.dtype != torch.int32 or serr.dim() != 3 or \
+                (serr.numel() and serr.stride(-1) != 1):
+            raise ValueError("serr must be a [B, Hkv, m] int32 tensor, innermost dimension contiguous")
+        _extent(serr, "serr", (B, Hkv, None))
+        m = serr.shape[-1]
+        if m > N:
+            raise ValueError(f"serr holds m={m} keys per head, more than N={N}")
+        _exact_out(added_out, "added_out", torch.int32, (B, Hkv, m))
+    elif added_out is not None:
+        raise ValueError("added_out needs serr")
+    if workspace is not None and (workspace.dtype != torch.uint8 or not workspace.is_contiguous()):
+        raise ValueError("workspace must be a contiguous uint8 tensor")
+    _on_gpu(q, K, V, codes, P, out, idx_out, score_out, qcode_out, serr, added_out, workspace)
     if sm_scale is None:
         sm_scale = 1.0 / math.sqrt(D)
     if out is None:
@@ -262,14 +381,6 @@ def decode_attention(q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, codes: t
             _ptr(idx_out), _ptr(score_out), _ptr(qcode_out), _ptr(workspace), workspace.numel(),
             _stream(stream)]
     if serr is not None:
-        if events is not None or score_out is not None or qcode_out is not None:
-            raise ValueError("serr cannot be combined with events, score_out or qcode_out")
-        if serr.dtype != torch.int32 or serr.dim() != 3 or serr.stride(-1) != 1 or serr.device != q.device:
-            raise ValueError("serr must be a [B, Hkv, m] int32 tensor on the GPU, innermost dimension contiguous")
-        m = serr.shape[-1]
-        if added_out is not None and (added_out.dtype != torch.int32 or not added_out.is_contiguous()
-                                      or tuple(added_out.shape) != (B, Hkv, m)):
-            raise ValueError("added_out must be a contiguous [B, Hkv, m] int32 tensor")
         _check(_lib.bpc_decode_attention_eas(*args[:23], _ptr(serr), serr.stride(0), serr.stride(1), m, _ptr(out),
                                              _ptr(idx_out), _ptr(added_out), _ptr(workspace), workspace.numel(),
                                              _stream(stream)),
@@ -287,7 +398,6 @@ def decode_attention(q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, codes: t
     return out
 
 
-
 def decode_attention_per_head(q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, codes: torch.Tensor,
                               P: torch.Tensor, k: int, sm_scale: Optional[float] = None, N: Optional[int] = None, *,
                               out: Optional[torch.Tensor] = None, idx_out: Optional[torch.Tensor] = None,
@@ -297,24 +407,18 @@ def decode_attention_per_head(q: torch.Tensor, K: torch.Tensor, V: torch.Tensor,
     quantises its own projection, scores the codes of KV head j // G, takes
     its own top-k and attends over it.  Shapes as decode_attention, except
     idx_out [B, Hq, k], score_out [B, Hq, N], qcode_out [B, Hq, 8, L/32]."""
-    _need(q, "q", torch.bfloat16, 3)
-    _need(K, "K", torch.bfloat16, 4)
-    _need(V, "V", torch.bfloat16, 4)
-    if not q.is_contiguous():
-        raise ValueError("q must be contiguous")
-    B, Hq, D = q.shape
-    _, Hkv, Ncap, _ = K.shape
-    N = Ncap if N is None else N
-    _u32_codes(codes)
-    L, sPb, sPh = _proj(P, D)
+    B, Hq, Hkv, D, N, L, sPb, sPh = _decode_inputs(q, K, V, codes, P, k, N)
+    _exact_out(out, "out", torch.float32, (B, Hq, D))
+    _exact_out(idx_out, "idx_out", torch.int32, (B, Hq, k))
+    _exact_out(score_out, "score_out", torch.int32, (B, Hq, N))
+    _exact_out(qcode_out, "qcode_out", torch.int32, (B, Hq, 8, L // 32))
+    if workspace is not None and (workspace.dtype != torch.uint8 or not workspace.is_contiguous()):
+        raise ValueError("workspace must be a contiguous uint8 tensor")
+    _on_gpu(q, K, V, codes, P, out, idx_out, score_out, qcode_out, workspace)
     if sm_scale is None:
         sm_scale = 1.0 / math.sqrt(D)
     if out is None:
         out = torch.empty(B, Hq, D, dtype=torch.float32, device=q.device)
-    for t, name, shape in ((idx_out, "idx_out", (B, Hq, k)), (score_out, "score_out", (B, Hq, N)),
-                           (qcode_out, "qcode_out", (B, Hq, 8, L // 32))):
-        if t is not None and (t.dtype != torch.int32 or not t.is_contiguous() or tuple(t.shape) != shape):
-            raise ValueError(f"{name} must be a contiguous int32 tensor of shape {shape}")
     ws_bytes = decode_per_head_workspace_bytes(B, Hq, Hkv, N, L, k, D)
     if workspace is None:
         workspace = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=q.device)
@@ -324,6 +428,7 @@ def decode_attention_per_head(q: torch.Tensor, K: torch.Tensor, V: torch.Tensor,
         _ptr(qcode_out), _ptr(workspace), workspace.numel(), _stream(stream)), "bpc_decode_attention_per_head")
     return out
 
+
 def select_hard(err: torch.Tensor, m: int, N: Optional[int] = None, *, serr_out: Optional[torch.Tensor] = None,
                 stream=None) -> torch.Tensor:
     """The error-aware safeguard's hard-to-hash set: per (b, KV head), the m
@@ -332,10 +437,14 @@ def select_hard(err: torch.Tensor, m: int, N: Optional[int] = None, *, serr_out:
     _need(err, "err", torch.float32, 3)
     B, Hkv, Ncap = err.shape
     N = Ncap if N is None else N
+    if not 1 <= N <= Ncap:
+        raise ValueError(f"N={N} must satisfy 1 <= N <= {Ncap}")
+    if not 0 <= m <= N:
+        raise ValueError(f"m={m} must satisfy 0 <= m <= N={N}")
+    _exact_out(serr_out, "serr_out", torch.int32, (B, Hkv, m))
+    _on_gpu(err, serr_out)
     if serr_out is None:
-        serr_out = torch.empty(B, Hkv, max(m, 0), dtype=torch.int32, device=err.device)
-    elif serr_out.dtype != torch.int32 or not serr_out.is_contiguous() or tuple(serr_out.shape) != (B, Hkv, m):
-        raise ValueError("serr_out must be a contiguous [B, Hkv, m] int32 tensor")
+        serr_out = torch.empty(B, Hkv, m, dtype=torch.int32, device=err.device)
     _check(_lib.bpc_select_hard(_ptr(err), err.stride(0), err.stride(1), B, Hkv, N, m, _ptr(serr_out),
                                 _stream(stream)),
            "bpc_select_hard")
@@ -348,17 +457,23 @@ def append_kv(k_new: torch.Tensor, v_new: torch.Tensor, K: torch.Tensor, V: torc
     """Decode-time append: store k_new, v_new [B, Hkv, T, 128] bf16 at rows
     [pos, pos + T) of the caches K, V [B, Hkv, Ncap, 128] and their codes
     (Algorithm 2 against P, [B, Hkv, L, 128] or a shared [L, 128]) at the same
-    rows of codes [B, Hkv, Ncap, L/32]."""
+    rows of codes [B, Hkv, Ncap, L/32].  err_out, when given, is a
+    contiguous [B, Hkv, T] fp32 tensor."""
     for t, nm in ((k_new, "k_new"), (v_new, "v_new"), (K, "K"), (V, "V")):
         _need(t, nm, torch.bfloat16, 4)
     B, Hkv, T, D = k_new.shape
-    if tuple(v_new.shape) != (B, Hkv, T, D):
-        raise ValueError("v_new must have the shape of k_new")
+    _extent(v_new, "v_new", (B, Hkv, T, D))
     Ncap = K.shape[2]
-    if tuple(K.shape[:2]) != (B, Hkv) or tuple(V.shape[:3]) != (B, Hkv, Ncap):
-        raise ValueError("K and V must be [B, Hkv, Ncap, D] with the batch and heads of k_new")
+    _extent(K, "K", (B, Hkv, Ncap, D))
+    _extent(V, "V", (B, Hkv, ("ge", Ncap), D))
+    if T < 1 or pos < 0 or pos + T > Ncap:
+        raise ValueError(f"pos={pos}, T={T}: the new rows must lie within the {Ncap} cache rows")
+    L, sPb, sPh = _proj(P, D, B, Hkv)
     _u32_codes(codes)
-    L, sPb, sPh = _proj(P, D)
+    _extent(codes, "codes", (B, Hkv, ("ge", pos + T), L // 32))
+    _exact_out(err_out, "err_out", torch.float32, (B, Hkv, T))
+    _fragile(fragile)
+    _on_gpu(k_new, v_new, K, V, codes, P, err_out, fragile)
     _check(_lib.bpc_append_kv(_ptr(k_new), *_kv_strides(k_new), _ptr(v_new), *_kv_strides(v_new), _ptr(K),
                               *_kv_strides(K), _ptr(V), *_kv_strides(V), _ptr(codes), codes.stride(0),
                               codes.stride(1), _ptr(P), sPb, sPh, B, Hkv, Ncap, pos, T, D, L, _ptr(err_out),
@@ -379,6 +494,12 @@ def dense_attention(q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, sm_scale:
     B, Hq, D = q.shape
     _, Hkv, Ncap, _ = K.shape
     N = Ncap if N is None else N
+    _extent(K, "K", (B, Hkv, ("ge", N), D))
+    _extent(V, "V", (B, Hkv, ("ge", N), D))
+    if not 1 <= N or Hq % Hkv:
+        raise ValueError(f"N={N} must be >= 1 and Hq={Hq} a multiple of Hkv={Hkv}")
+    _exact_out(out, "out", torch.float32, (B, Hq, D))
+    _on_gpu(q, K, V, out, workspace)
     if sm_scale is None:
         sm_scale = 1.0 / math.sqrt(D)
     if out is None:

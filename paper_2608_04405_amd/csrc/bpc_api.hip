@@ -229,7 +229,7 @@ static int decode_impl(const uint16_t* q, const uint16_t* K, int64_t sK_b, int64
                        int Hkv, int N, int D, int L, int k, float sm_scale, float* out, int32_t* idx_out,
                        int32_t* score_out, uint32_t* qcode_out, const int32_t* serr, int64_t sS_b, int64_t sS_h,
                        int m, int32_t* added_out, void* workspace, size_t workspace_bytes, void* stream,
-                       void* const* events, int n_events) {
+                       void* const* events, int n_events, bool launch = true) {
   g_last_error[0] = 0;
   int st;
   if ((st = check_sizes(B, Hkv, N))) return st;
@@ -263,6 +263,7 @@ static int decode_impl(const uint16_t* q, const uint16_t* K, int64_t sK_b, int64
   if (m > 0) {
     if (!serr) return fail(BPC_EINVAL, "serr is required when m > 0");
     if (sS_b < 0 || sS_h < 0) return fail(BPC_EINVAL, "serr strides must be >= 0");
+    if (!aligned4(serr)) return fail(BPC_EALIGN, "serr must be 4-byte aligned");
     if ((st = check_opt_aligned("added_out", added_out))) return st;
   }
   if (events && n_events != BPC_DECODE_STAGES + 1)
@@ -272,6 +273,7 @@ static int decode_impl(const uint16_t* q, const uint16_t* K, int64_t sK_b, int64
     return fail(BPC_EWORKSPACE, "workspace of %zu bytes given, %zu needed", workspace ? workspace_bytes : 0,
                 lay.total);
   if (reinterpret_cast<uintptr_t>(workspace) & 255u) return fail(BPC_EALIGN, "workspace must be 256-byte aligned");
+  if (!launch) return BPC_OK;
 
   DecodeArgs a{};
   a.q = q;
@@ -350,15 +352,25 @@ int bpc_decode_attention_per_head(const uint16_t* q, const uint16_t* K, int64_t 
   const int calls = linear ? 1 : B;
   const int Bc = linear ? B * Hkv : Hkv;  // sequences b' per call
   const int W = L / 32;
-  for (int c = 0; c < calls; ++c) {
-    st = decode_impl(q + (size_t)c * Hq * kHeadDim, K + c * sK_b, sK_h, 0, sK_n, V + c * sV_b, sV_h, 0, sV_n,
-                     codes + c * sC_b, sC_h, 0, P + c * sP_b, sP_h, 0, Bc, G, G, N, D, L, k, sm_scale,
-                     out + (size_t)c * Hq * kHeadDim, idx_out ? idx_out + (size_t)c * Hq * k : nullptr,
-                     score_out ? score_out + (size_t)c * Hq * N : nullptr,
-                     qcode_out ? qcode_out + (size_t)c * Hq * 8 * W : nullptr, nullptr, 0, 0, 0, nullptr, workspace,
-                     workspace_bytes, stream, nullptr, 0);
-    if (st) return st;
-  }
+  // every call's offset pointers are checked (alignment included) before
+  // the first one launches, so that an error leaves every output untouched
+  for (int pass = 0; pass < 2; ++pass)
+    for (int c = 0; c < calls; ++c) {
+      st = decode_impl(q + (size_t)c * Hq * kHeadDim, K + c * sK_b, sK_h, 0, sK_n, V + c * sV_b, sV_h, 0, sV_n,
+                       codes + c * sC_b, sC_h, 0, P + c * sP_b, sP_h, 0, Bc, G, G, N, D, L, k, sm_scale,
+                       out + (size_t)c * Hq * kHeadDim, idx_out ? idx_out + (size_t)c * Hq * k : nullptr,
+                       score_out ? score_out + (size_t)c * Hq * N : nullptr,
+                       qcode_out ? qcode_out + (size_t)c * Hq * 8 * W : nullptr, nullptr, 0, 0, 0, nullptr,
+                       workspace, workspace_bytes, stream, nullptr, 0, pass == 1);
+      if (st) {
+        if (calls > 1) {
+          char detail[sizeof(g_last_error)];
+          snprintf(detail, sizeof(detail), "%s", g_last_error);
+          return fail(st, "sequence %d of %d (one call per sequence): %s", c, calls, detail);
+        }
+        return st;
+      }
+    }
   return BPC_OK;
 }
 

@@ -1212,7 +1212,9 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(G 
         const int kin = key[u] - n0;
         const bool here = key[u] >= n0 && kin < cnt;
         add[u] = here && !((sh.sel[kin >> 5] >> (kin & 31)) & 1u);
-        if (here && added_out) added_out[(size_t)bh * m + j] = add[u];
+        // an entry outside [0, N) lies in no slice: slice 0 marks it as not added
+        const bool outside = j < m && (key[u] < 0 || key[u] >= N);
+        if (added_out && (here || (outside && s == 0))) added_out[(size_t)bh * m + j] = add[u];
         na += add[u];
       }
       int tot;

@@ -121,6 +121,26 @@ def pin_alg1_worked_example(o):
     assert fr == g["fragile_padded"]
 
 
+def pin_decode_worked_example(o):
+    # the decode step of the hand-worked example: query planes, scores
+    # [254, 0, 0, -254], the top-2 with its tie at 0 going to key 1, and the
+    # two-key softmax output (closed form in the fixture)
+    g = _golden()
+    L = g["L_padded"]
+    K = to_bf16_bits(_pad(g["K_small"], 128))
+    V = to_bf16_bits(_pad(g["V_small"], 128))
+    q = to_bf16_bits(_pad([g["query"]], 128))
+    P = np.zeros((L, 128), np.float32)
+    P[:2, :4] = np.asarray(g["P_small"], np.float32)
+    codes = np.asarray(g["codes_padded"], np.uint32)[:, None]
+    r = o.decode_head(q, K, V, codes, P, g["k"], g["sm_scale"])
+    assert r["p"][:2].tolist() == g["p_padded_first2"] and np.all(r["p"][2:] == 0) and r["T"] == g["T"]
+    assert r["scores"].tolist() == g["scores"]
+    assert r["idx"].tolist() == g["topk"]
+    np.testing.assert_allclose(r["out"][0, :4], g["out_first4"], rtol=1e-14, atol=1e-15)
+    assert np.all(r["out"][0, 4:] == 0)
+
+
 def pin_alg1_rank1(o):
     rng = np.random.default_rng(6)
     N, D, L = 300, 128, 32

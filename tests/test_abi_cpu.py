@@ -311,3 +311,13 @@ def test_per_head_workspace_and_rejects(lib):
     assert call(ws_bytes=1024) == EWS
     assert call(k=0, ws_bytes=1 << 40) == EINVAL
     assert call(D=64, ws_bytes=1 << 40) == EUNSUP
+    # one call per sequence (batch stride != Hkv x head stride): a later
+    # sequence's codes pointer that is not 16-byte aligned is found before
+    # the first sequence launches (no HIP call is reached, so no EHIP here)
+    assert call(B=2, sCb=8 * 4096 + 1, ws_bytes=1 << 40) == EALIGN
+    assert b"sequence 1 of 2" in lib.bpc_last_error()
+
+
+def test_decode_eas_rejects_misaligned_serr(lib):
+    assert _decode_eas(lib, serr=FAKE + 2) == EALIGN
+    assert b"serr" in lib.bpc_last_error()

@@ -203,3 +203,32 @@ def test_decode_eas_window_miss():
     codes[0, 0, near] = planes[0]
     serr = np.sort(np.r_[near[:5], rng.choice(np.arange(20000, 30000), 20, replace=False)])[None, None]
     _eas_compare(q, K, V, codes, P, k, serr, label="eas window miss")
+
+
+def test_decode_eas_out_of_range_entries_ignored():
+    """Entries of S_err outside [0, N) lie in no slice: they are ignored and
+    their added flags are 0 (the rest as the oracle on the in-range set)."""
+    rng = np.random.default_rng(23)
+    B, Hq, Hkv, N, L, k = 1, 4, 2, 20000, 64, 200
+    q, K, V, codes, P = _random_case(rng, B, Hq, Hkv, N, L)
+    inside = np.stack([np.sort(rng.choice(N, 12, replace=False)) for _ in range(Hkv)])[None]
+    serr_np = np.concatenate([np.full((B, Hkv, 2), -1), inside, np.full((B, Hkv, 1), N),
+                              np.full((B, Hkv, 1), N + 1000)], axis=-1)
+    m = serr_np.shape[-1]
+    codes_t = torch.from_numpy(np.ascontiguousarray(codes).view(np.int32)).to(DEV)
+    serr = torch.from_numpy(serr_np.astype(np.int32)).to(DEV)
+    idx = torch.full((B, Hkv, k), -1, dtype=torch.int32, device=DEV)
+    added = torch.full((B, Hkv, m), 7, dtype=torch.int32, device=DEV)
+    sm = 1.0 / np.sqrt(128)
+    out = bpc.decode_attention(q, K, V, codes_t, torch.from_numpy(P).to(DEV), k, sm, idx_out=idx, serr=serr,
+                               added_out=added)
+    torch.cuda.synchronize()
+    G = Hq // Hkv
+    for h in range(Hkv):
+        ref = oracle.decode_head_eas(bits(q)[0, h * G:(h + 1) * G], bits(K)[0, h], bits(V)[0, h], codes[0, h],
+                                     P[0, h], k, inside[0, h], sm)
+        got = added[0, h].cpu().numpy()
+        assert np.array_equal(got[2:-2], ref["added"]) and np.all(got[:2] == 0) and np.all(got[-2:] == 0), got
+        assert np.array_equal(idx[0, h].cpu().numpy(), ref["idx"])
+        e = rel_err(out[0, h * G:(h + 1) * G].cpu().numpy(), ref["out"])
+        assert np.all(e <= TOL), e

@@ -406,9 +406,11 @@ def test_decode_profiled_events(tiny):
 
 
 def test_errors_raise():
-    with pytest.raises(bpc.BPCError):
-        q = torch.zeros(1, 4, 128, dtype=torch.bfloat16, device=DEV)
-        K = torch.zeros(1, 1, 10, 128, dtype=torch.bfloat16, device=DEV)
-        codes = torch.zeros(1, 1, 10, 1, dtype=torch.int32, device=DEV)
-        P = torch.zeros(1, 1, 32, 128, dtype=torch.float32, device=DEV)
-        bpc.decode_attention(q, K, K, codes, P, 11)  # k > N
+    q = torch.zeros(1, 4, 128, dtype=torch.bfloat16, device=DEV)
+    K = torch.zeros(1, 1, 10, 128, dtype=torch.bfloat16, device=DEV)
+    codes = torch.zeros(1, 1, 10, 1, dtype=torch.int32, device=DEV)
+    P = torch.zeros(1, 1, 32, 128, dtype=torch.float32, device=DEV)
+    with pytest.raises(ValueError):  # the binding's own checks: k > N
+        bpc.decode_attention(q, K, K, codes, P, 11)
+    with pytest.raises(bpc.BPCError):  # the library's: a group of 3 query heads
+        bpc.decode_attention(q[:, :3].contiguous(), K, K, codes, P, 4)

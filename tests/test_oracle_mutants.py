@@ -51,6 +51,8 @@ MUTANTS = {
     "perq_group_selection": ("heads = [decode_head(q_bits[g:g + 1], K_bits, V_bits, codes, P, k, sm_scale)",
                              "heads = [decode_head(q_bits, K_bits, V_bits, codes, P, k, sm_scale)"),
     "perq_first_head_only": ("heads = [decode_head(q_bits[g:g + 1], K_bits,", "heads = [decode_head(q_bits[0:1], K_bits,"),
+    "decode_attends_all": ("    out = attend(q_bits, K_bits, V_bits, idx, sm_scale)\n    return {\"p\"",
+                           "    out = attend(q_bits, K_bits, V_bits, np.arange(len(c)), sm_scale)\n    return {\"p\""),
     "perq_head_order": ("for g in range(q_bits.shape[0])]", "for g in range(q_bits.shape[0])][::-1]"),
 }
 

@@ -23,7 +23,11 @@ Random numbers come from torch generators seeded per (config, layer, batch,
 head, tensor) so that any single head can be regenerated on its own.  The
 values depend on the device the generator runs on (CPU and GPU streams
 differ), so a caller that needs the same head on both sides generates it once
-and copies it.
+and copies it.  On the CPU they do not depend on the host: the normals are
+drawn in float64 (torch's float32 normals take a vectorised path whose values
+change with the CPU's instruction set) and Z A is accumulated elementwise in
+a fixed order (a BLAS product's summation order changes with the CPU), so
+values stored from one machine are reproduced on another.
 """
 
 from __future__ import annotations
@@ -147,41 +151,77 @@ def make_gaussian_directions(cfg: DecodeConfig, L: Optional[int] = None) -> torc
     return torch.randn(L, cfg.D, generator=g, dtype=torch.float64).to(torch.float32)
 
 
+def _normals(shape, g, device) -> torch.Tensor:
+    """float64 standard normals (host-independent on the CPU, see above)."""
+    return torch.randn(shape, generator=g, device=device, dtype=torch.float64)
+
+
+def _to_bf16(x: torch.Tensor) -> torch.Tensor:
+    """float64 -> float32 (round to nearest even) -> bf16 (round to nearest even)."""
+    return x.to(torch.float32).to(torch.bfloat16)
+
+
 def _key_basis(cfg: DecodeConfig, layer: int, h: int, device):
     g = _generator(device, cfg.seed, _TAG_BASIS, layer, h)
-    A = torch.randn(cfg.rank, cfg.D, generator=g, device=device, dtype=torch.float32)
+    A = _normals((cfg.rank, cfg.D), g, device)
     perm = torch.randperm(cfg.D, generator=g, device=device)
     return A, perm[: cfg.n_outliers]
 
 
 def make_query(cfg: DecodeConfig, layer: int = 0, device="cpu") -> torch.Tensor:
     g = _generator(device, cfg.seed, _TAG_QUERY, layer)
-    q = torch.randn(cfg.B, cfg.Hq, cfg.D, generator=g, device=device, dtype=torch.float32)
-    return q.to(torch.bfloat16)
+    return _to_bf16(_normals((cfg.B, cfg.Hq, cfg.D), g, device))
+
+
+_CHUNK = 65536  # rows per independently seeded block of normals
+
+
+def _rows_of_head(cfg: DecodeConfig, A: torch.Tensor, outl: torch.Tensor, layer: int, b: int, h: int,
+                  c: int, device):
+    """K and V rows [c * _CHUNK, ...) of one head, bf16.  Each block of rows
+    has generators of its own, so blocks can be drawn in parallel."""
+    rows = min(_CHUNK, cfg.N - c * _CHUNK)
+    gk = _generator(device, cfg.seed, _TAG_KEYS, layer, b, h, c)
+    Z = _normals((rows, cfg.rank), gk, device)
+    K = _normals((rows, cfg.D), gk, device).mul_(cfg.noise)
+    # K = noise E + Z A, the rank terms added in ascending order, each product
+    # and sum rounded separately (no fused multiply-add, no BLAS)
+    for r in range(cfg.rank):
+        K.add_(Z[:, r:r + 1] * A[r])
+    K[:, outl] *= cfg.outlier_scale
+    gv = _generator(device, cfg.seed, _TAG_VALUES, layer, b, h, c)
+    return _to_bf16(K), _to_bf16(_normals((rows, cfg.D), gv, device))
 
 
 def make_head(cfg: DecodeConfig, q: torch.Tensor, layer: int, b: int, h: int,
               device="cpu", needle_mode: str = "rho", basis=None):
     """K, V [N, D] bf16 and needle positions for one (layer, sequence, KV head)."""
     A, outl = basis if basis is not None else _key_basis(cfg, layer, h, device)
-    gk = _generator(device, cfg.seed, _TAG_KEYS, layer, b, h)
-    Z = torch.randn(cfg.N, cfg.rank, generator=gk, device=device, dtype=torch.float32)
-    E = torch.randn(cfg.N, cfg.D, generator=gk, device=device, dtype=torch.float32)
-    K = torch.addmm(E, Z, A, beta=cfg.noise, alpha=1.0)
-    del Z, E
-    K[:, outl] *= cfg.outlier_scale
-    K = K.to(torch.bfloat16)
-    gv = _generator(device, cfg.seed, _TAG_VALUES, layer, b, h)
-    V = torch.randn(cfg.N, cfg.D, generator=gv, device=device, dtype=torch.float32).to(torch.bfloat16)
+    K = torch.empty(cfg.N, cfg.D, dtype=torch.bfloat16, device=device)
+    V = torch.empty_like(K)
+    nblk = (cfg.N + _CHUNK - 1) // _CHUNK
+
+    def fill(c):
+        Kc, Vc = _rows_of_head(cfg, A, outl, layer, b, h, c, device)
+        K[c * _CHUNK:c * _CHUNK + Kc.shape[0]] = Kc
+        V[c * _CHUNK:c * _CHUNK + Vc.shape[0]] = Vc
+
+    if torch.device(device).type == "cpu" and nblk > 1:
+        import concurrent.futures as cf
+        with cf.ThreadPoolExecutor(max_workers=min(nblk, max(1, min(16, torch.get_num_threads())))) as ex:
+            list(ex.map(fill, range(nblk)))
+    else:
+        for c in range(nblk):
+            fill(c)
     pos = torch.empty(0, dtype=torch.int64, device=device)
     if cfg.needles > 0:
         gn = _generator(device, cfg.seed, _TAG_NEEDLE, layer, b, h)
         pos = torch.randperm(cfg.N, generator=gn, device=device)[: cfg.needles]
-        Kf = K.float()
+        Kf = K.double()
         rho = torch.sqrt((Kf * Kf).sum(dim=1).mean())
         Gq = cfg.G
         for j in range(cfg.needles):
-            qg = q[b, h * Gq + (j % Gq)].float()
+            qg = q[b, h * Gq + (j % Gq)].double()
             unit = qg / torch.linalg.vector_norm(qg)
             if needle_mode == "rho":
                 vec = 3.0 * rho * unit
@@ -191,7 +231,7 @@ def make_head(cfg: DecodeConfig, q: torch.Tensor, layer: int, b: int, h: int,
                 vec = 3.0 * qg
             else:
                 raise ValueError(needle_mode)
-            K[pos[j]] = vec.to(torch.bfloat16)
+            K[pos[j]] = _to_bf16(vec)
     return K, V, pos
 
 
