@@ -50,6 +50,8 @@ def parse():
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run a plain 1 GiB device copy (counter calibration for rocprofv3 --pmc)")
     ap.add_argument("--cpu-sample-heads", type=int, default=128)
+    ap.add_argument("--decode-path", choices=("auto", "three-launch"), default="auto",
+                    help="auto: one fused launch when the step's workgroups fit on the GPU at once")
     ap.add_argument("--summarize", metavar="DIR", nargs="+", default=None,
                     help="summarize rocprofv3 csv output under each DIR (kernel stats and counters per dispatch) "
                          "instead of benchmarking")
@@ -180,6 +182,7 @@ def main():
 
     cfg = config_by_name("batch16_128k")
     dev = torch.device("cuda:0")
+    bpc.set_decode_path(0 if args.decode_path == "auto" else 1)
     B, Hq, Hkv, D, N, L, k = cfg.B, cfg.Hq, cfg.Hkv, cfg.D, cfg.N, cfg.L, cfg.k
     sm = 1.0 / math.sqrt(D)
     W = L // 32
@@ -221,7 +224,7 @@ def main():
     torch.cuda.empty_cache()
     log(f"prefill {prefill}")
 
-    ws = torch.empty(bpc.decode_workspace_bytes(B, Hq, Hkv, N, L, k), dtype=torch.uint8, device=dev)
+    ws = torch.zeros(bpc.decode_workspace_bytes(B, Hq, Hkv, N, L, k), dtype=torch.uint8, device=dev)
     outs = [torch.empty(B, Hq, D, dtype=torch.float32, device=dev) for _ in insts]
 
     def step(j, events=None):
@@ -316,7 +319,7 @@ def main():
 
         fixed = {}
         for kb in (1024, 2048):
-            ws_b = torch.empty(bpc.decode_workspace_bytes(B, Hq, Hkv, N, L, kb), dtype=torch.uint8, device=dev)
+            ws_b = torch.zeros(bpc.decode_workspace_bytes(B, Hq, Hkv, N, L, kb), dtype=torch.uint8, device=dev)
 
             def fixed_step(j, kb=kb, ws_b=ws_b):
                 it = insts[j % len(insts)]
@@ -329,7 +332,7 @@ def main():
         log(f"fixed budgets: {fixed}")
 
         # ---------------------------------------------------------------- per-query-head selection (context)
-        ws_ph = torch.empty(bpc.decode_per_head_workspace_bytes(B, Hq, Hkv, N, L, k), dtype=torch.uint8, device=dev)
+        ws_ph = torch.zeros(bpc.decode_per_head_workspace_bytes(B, Hq, Hkv, N, L, k), dtype=torch.uint8, device=dev)
 
         def per_head_step(j):
             it = insts[j % len(insts)]

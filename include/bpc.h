@@ -74,6 +74,17 @@ const char* bpc_last_error(void);
 int bpc_version(void);
 
 /*
+ * bpc_set_decode_path -- how the decode entry points run a step, for this
+ * process: 0 (the default) runs it as one fused launch whenever every
+ * workgroup of the step fits on the current device at once, else as three
+ * launches; 1 always uses the three launches (for comparisons and tests).
+ * Calls already enqueued are not affected; workspace sizes follow the path
+ * (bpc_decode_workspace_bytes queries it).  Returns BPC_EINVAL for any other
+ * value.
+ */
+int bpc_set_decode_path(int path);
+
+/*
  * bpc_build_hash -- binary principal components of each (sequence, KV
  * head)'s keys (Sec. 3.2, "Binary Principal Components Finding", Algorithm
  * "Constructing hash codes and corresponding hashing projection"; the
@@ -198,12 +209,22 @@ int bpc_append_kv(const uint16_t* k_new, int64_t sKn_b, int64_t sKn_h, int64_t s
  * score_out  [B, Hkv, N] int32 scores c_n (or NULL)
  * qcode_out  [B, Hkv, 8, W] uint32 packed query planes (or NULL)
  * workspace  at least bpc_decode_workspace_bytes(...) bytes, 256-byte
- *            aligned; contents on entry do not matter.  Two calls that use
- *            the same workspace must be ordered on one stream.
- * Cost: three kernel launches (query packing with scoring, threshold with
- * selection and attention, merge of the per-slice partials), plus one for a
- * ragged last slice or codes whose strides are not multiples of 4 words.
+ *            aligned.  Its first 256 KiB (BPC_DECODE_ZEROED_BYTES) must be
+ *            zero before the first call on it (allocate it zeroed); every
+ *            call leaves them zero.  The rest may hold anything.  Two calls
+ *            that use the same workspace must be ordered on one stream.
+ *            The size depends on the path the current device takes (below).
+ * Cost: when every workgroup of the step fits on the device at once (a
+ * slice of 16384 keys per workgroup; e.g. 1024 slices at L = 64 and G <= 4
+ * on MI355X), one fused launch: each slice is packed and scored, the slices
+ * of a (b, h) exchange their histogram summaries through the workspace,
+ * select, gather and attend, and the last slice of (b, h) merges the
+ * partials.  Otherwise three launches (query packing with scoring, threshold
+ * with selection and attention, merge of the per-slice partials), plus one
+ * for a ragged last slice or codes whose strides are not multiples of 4
+ * words.  bpc_set_decode_path selects the three launches for comparisons.
  */
+#define BPC_DECODE_ZEROED_BYTES (256u * 1024u)
 size_t bpc_decode_workspace_bytes(int B, int Hq, int Hkv, int N, int D, int L, int k);
 int bpc_decode_attention(const uint16_t* q,
                          const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t sK_n,

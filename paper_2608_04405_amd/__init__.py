@@ -32,6 +32,8 @@ __all__ = [
     "DECODE_STAGES",
     "DECODE_STAGE_NAMES",
     "version",
+    "set_decode_path",
+    "DECODE_ZEROED_BYTES",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libbpc.so")
@@ -80,11 +82,16 @@ _lib.bpc_dense_attention.argtypes = [_p, _p, _i64, _i64, _i64, _p, _i64, _i64, _
                                      ctypes.c_float, _p, _p, _sz, _p]
 _lib.bpc_select_hard.restype = _i
 _lib.bpc_select_hard.argtypes = [_p, _i64, _i64, _i, _i, _i, _i, _p, _p]
+_lib.bpc_set_decode_path.restype = _i
+_lib.bpc_set_decode_path.argtypes = [_i]
 _lib.bpc_decode_attention_profiled.restype = _i
 _lib.bpc_decode_attention_profiled.argtypes = _DECODE_ARGS + [ctypes.POINTER(_p), _i]
 
 DECODE_STAGES = 3
 DECODE_STAGE_NAMES = ("score", "attend", "merge")
+# a decode workspace's leading bytes that must be zero before its first use
+# (the fused path's arrival counters; every call leaves them zero)
+DECODE_ZEROED_BYTES = 256 * 1024
 
 
 class BPCError(RuntimeError):
@@ -102,6 +109,12 @@ def _check(status: int, where: str) -> None:
 
 def version() -> int:
     return _lib.bpc_version()
+
+
+def set_decode_path(path: int) -> None:
+    """0: a decode step runs as one fused launch whenever its workgroups fit
+    on the GPU at once (the default); 1: always the three launches."""
+    _check(_lib.bpc_set_decode_path(int(path)), "bpc_set_decode_path")
 
 
 def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
@@ -375,7 +388,7 @@ def decode_attention(q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, codes: t
         out = torch.empty(B, Hq, D, dtype=torch.float32, device=q.device)
     ws_bytes = decode_workspace_bytes(B, Hq, Hkv, N, L, k, D)
     if workspace is None:
-        workspace = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=q.device)
+        workspace = torch.zeros(max(ws_bytes, 1), dtype=torch.uint8, device=q.device)
     args = [_ptr(q), _ptr(K), *_kv_strides(K), _ptr(V), *_kv_strides(V), _ptr(codes), codes.stride(0),
             codes.stride(1), _ptr(P), sPb, sPh, B, Hq, Hkv, N, D, L, k, float(sm_scale), _ptr(out),
             _ptr(idx_out), _ptr(score_out), _ptr(qcode_out), _ptr(workspace), workspace.numel(),
@@ -421,7 +434,7 @@ def decode_attention_per_head(q: torch.Tensor, K: torch.Tensor, V: torch.Tensor,
         out = torch.empty(B, Hq, D, dtype=torch.float32, device=q.device)
     ws_bytes = decode_per_head_workspace_bytes(B, Hq, Hkv, N, L, k, D)
     if workspace is None:
-        workspace = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=q.device)
+        workspace = torch.zeros(max(ws_bytes, 1), dtype=torch.uint8, device=q.device)
     _check(_lib.bpc_decode_attention_per_head(
         _ptr(q), _ptr(K), *_kv_strides(K), _ptr(V), *_kv_strides(V), _ptr(codes), codes.stride(0), codes.stride(1),
         _ptr(P), sPb, sPh, B, Hq, Hkv, N, D, L, k, float(sm_scale), _ptr(out), _ptr(idx_out), _ptr(score_out),

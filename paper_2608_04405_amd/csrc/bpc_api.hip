@@ -78,6 +78,7 @@ DecodeLayout decode_layout(int B, int Hq, int Hkv, int N, int L, int k) {
   d.W = L / 32;
   d.G = Hq / Hkv;
   d.nslices = (N + kSlice - 1) / kSlice;
+  d.fused = decode_fused_ok(B, Hq, Hkv, N, L);
   const size_t S = BH * d.nslices;
   size_t o = 0;
   auto take = [&](size_t bytes) {
@@ -85,6 +86,14 @@ DecodeLayout decode_layout(int B, int Hq, int Hkv, int N, int L, int k) {
     o = align_up(o + bytes, 256);
     return at;
   };
+  d.off_sync = take(kSyncRegionBytes);  // both paths; only the fused one uses it
+  if (d.fused) {
+    d.off_pub = take(S * kFusedPubWords * sizeof(uint32_t));
+    d.off_part = take(S * d.G * (kHeadDim + 2) * sizeof(float));
+    d.off_rows = take(BH * (size_t)k * sizeof(int32_t));
+    d.total = o;
+    return d;
+  }
   d.off_cand = take(S * (size_t)kSlice * sizeof(uint32_t));
   d.off_meta = take(S * 4 * sizeof(uint32_t));
   d.off_hist_fine = take(S * (size_t)fine_stride(L) * sizeof(uint32_t));
@@ -137,7 +146,13 @@ const char* bpc_status_string(int status) {
 
 const char* bpc_last_error(void) { return g_last_error; }
 
-int bpc_version(void) { return 100; }
+int bpc_version(void) { return 200; }
+
+int bpc_set_decode_path(int path) {
+  if (path != 0 && path != 1) return fail(BPC_EINVAL, "path=%d must be 0 (automatic) or 1 (three launches)", path);
+  decode_set_path(path);
+  return BPC_OK;
+}
 
 size_t bpc_build_workspace_bytes(int B, int Hkv, int N, int D, int L) {
   if (B < 1 || Hkv < 1 || N < 1 || D != kHeadDim) return 0;
@@ -288,7 +303,7 @@ static int decode_impl(const uint16_t* q, const uint16_t* K, int64_t sK_b, int64
   a.ws = static_cast<char*>(workspace);
   a.stream = static_cast<hipStream_t>(stream);
   a.events = reinterpret_cast<hipEvent_t const*>(events);
-  hipError_t e = launch_decode(a);
+  hipError_t e = launch_decode(a, lay);
   if (e != hipSuccess) return hip_fail(e, "bpc_decode_attention launch");
   return BPC_OK;
 }

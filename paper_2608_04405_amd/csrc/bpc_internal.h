@@ -47,6 +47,18 @@ constexpr int kWinBins = 128;
 constexpr int kWinRec = 4 + kWinBins / 2;  // u32 per record
 constexpr int kWinSlices = 64;             // slices per (b, h) the one-round threshold handles
 
+// Fused single-kernel decode (all slices of the grid resident at once): per
+// (b, h) kFusedSyncWords u32 of arrival counters (zero between calls), per
+// slice kFusedPubWords u32 of published threshold data and G (max, sum,
+// o[128]) partials, per (b, h) a row list of k ints for rows past the LDS list.
+constexpr int kFusedSyncWords = 16;
+constexpr int kFusedPubWords = kWinRec + 4 + kCoarseStride + 128;
+// The counters sit in a fixed region at the start of every decode workspace
+// (either path), for up to kFusedMaxBH (b, h) pairs; the three-launch path
+// never writes it, so it stays zero once zeroed.
+constexpr int kFusedMaxBH = 4096;
+constexpr size_t kSyncRegionBytes = (size_t)kFusedMaxBH * kFusedSyncWords * sizeof(uint32_t);
+
 // ---- build tiling ----------------------------------------------------------
 constexpr int kBuildGroups = 2;                  // groups of 64 keys per build workgroup
 constexpr int kBuildThreads = 256 * kBuildGroups;  // four wavefronts (coordinate blocks) per group
@@ -63,9 +75,17 @@ constexpr int kBuildChunk = 64 * kBuildGroups;     // keys per workgroup (one ch
 // LDS list holds, the attention kernel writes them over the slice's own
 // candidate area (a kept entry's rank never exceeds its position there).
 constexpr int kQcodeStride = 64;
+// Both paths begin with the counter region (kSyncRegionBytes, zero before
+// the first call on the workspace, left zero by every call).  The fused
+// path's workspace (fused = true) then holds arrival counters [B Hkv]
+// [kFusedSyncWords] u32 (inside the region), published records [slices]
+// [kFusedPubWords] u32, partials [slices][G][130] fp32 and row lists
+// [B Hkv][k] int32.
 struct DecodeLayout {
+  bool fused;
   int nslices, G, W;
   size_t off_cand, off_meta, off_hist_fine, off_hist_cc, off_win, off_part, off_qcode, total;
+  size_t off_sync, off_pub, off_rows;
 };
 
 struct BuildLayout {
@@ -74,6 +94,11 @@ struct BuildLayout {
 };
 
 DecodeLayout decode_layout(int B, int Hq, int Hkv, int N, int L, int k);
+// Whether the current device runs the decode step as the single fused
+// launch: every slice's workgroup must be resident at once.
+bool decode_fused_ok(int B, int Hq, int Hkv, int N, int L);
+// 0: automatic; 1: always the three-launch path
+void decode_set_path(int path);
 BuildLayout build_layout(int B, int Hkv, int N, int L);
 
 // ---- launchers (enqueue only; arguments already validated) ---------------
@@ -102,7 +127,7 @@ struct DecodeArgs {
   hipEvent_t const* events;  // BPC_DECODE_STAGES + 1 handles, or nullptr
 };
 
-hipError_t launch_decode(const DecodeArgs& a);
+hipError_t launch_decode(const DecodeArgs& a, const DecodeLayout& lay);
 
 // dense decode attention (full softmax over all N keys), the comparison point
 struct DenseArgs {

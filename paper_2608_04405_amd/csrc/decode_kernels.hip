@@ -27,6 +27,8 @@
 // candidates contain every selected key and every histogram bin at or below
 // T* is written by every slice.
 
+#include <atomic>
+
 #include "bpc_internal.h"
 
 namespace bpc {
@@ -93,10 +95,10 @@ __device__ __forceinline__ void slice_tile(int id, int BH, int nslices, int& bh,
 // add would.  The group sum is quantised to [-127, 127] (scale 127 / max |x|,
 // rounded half away from zero) and packed into 1 sign + 7 magnitude planes.
 // ---------------------------------------------------------------------------
-template <int L>
+template <int L, int GMAX = kMaxGroup>
 struct QpackShared {
-  float4 P[L * 32];                  // P, 16-byte units in the swizzled order above
-  uint4 q[kMaxGroup][kHeadDim / 8];  // the group's queries, bf16
+  float4 P[L * 32];             // P, 16-byte units in the swizzled order above
+  uint4 q[GMAX][kHeadDim / 8];  // the group's queries, bf16 (at most GMAX heads)
 };
 
 // small per-workgroup state of the packing (kept outside the histogram)
@@ -134,18 +136,24 @@ __device__ __forceinline__ uint32_t every_fourth_bit(unsigned long long m) {
 // 0 = signs, plane 1 + j = bit j of |p|).  after_loads() runs right after
 // the P and query loads are issued, so that the caller can put loads of its
 // own in flight behind them.  Ends with a barrier; sh is free after it.
-template <int L, int NT, class AfterLoads>
-__device__ __forceinline__ void qpack_block(QpackShared<L>& sh, QpackOut<L>& o, const uint16_t* __restrict__ qg,
+template <int L, int NT, int GMAX, class AfterLoads>
+__device__ __forceinline__ void qpack_block(QpackShared<L, GMAX>& sh, QpackOut<L>& o, const uint16_t* __restrict__ qg,
                                             const float* __restrict__ Pbh, int G, AfterLoads&& after_loads) {
-  static_assert((L * 32) % NT == 0 && 4 * L <= NT, "thread count");
-  constexpr int PV = L * 32 / NT;  // 16-byte units of P per thread
+  static_assert((L * 32) % NT == 0 && NT % 64 == 0, "thread count");
+  constexpr int PV = L * 32 / NT;                // 16-byte units of P per thread
+  constexpr int RP = (4 * L + NT - 1) / NT;      // passes over the rows (a quad of lanes per row)
+  constexpr int ACTW = (4 * L < NT ? 4 * L : NT) / 64;  // wavefronts holding rows
   const int t = threadIdx.x, lane = t & 63, wid = t >> 6;
   {
     float4 pv[PV];
 #pragma unroll
     for (int r = 0; r < PV; ++r) pv[r] = reinterpret_cast<const float4*>(Pbh)[t + NT * r];
-    uint4 qv = make_uint4(0u, 0u, 0u, 0u);
-    if (t < G * (kHeadDim / 8)) qv = reinterpret_cast<const uint4*>(qg)[t];
+    uint4 qv[(GMAX * (kHeadDim / 8) + NT - 1) / NT];
+#pragma unroll
+    for (int r = 0; r < (GMAX * (kHeadDim / 8) + NT - 1) / NT; ++r) {
+      const int e = t + NT * r;
+      qv[r] = (e < G * (kHeadDim / 8)) ? reinterpret_cast<const uint4*>(qg)[e] : make_uint4(0u, 0u, 0u, 0u);
+    }
     after_loads();
 #pragma unroll
     for (int r = 0; r < PV; ++r) {
@@ -153,52 +161,62 @@ __device__ __forceinline__ void qpack_block(QpackShared<L>& sh, QpackOut<L>& o, 
       const int i = f >> 5, c = (f >> 3) & 3, u = f & 7;
       sh.P[i * 32 + c * 8 + (u ^ qpack_swz(i, c))] = pv[r];
     }
-    if (t < G * (kHeadDim / 8)) sh.q[t / (kHeadDim / 8)][t % (kHeadDim / 8)] = qv;
+#pragma unroll
+    for (int r = 0; r < (GMAX * (kHeadDim / 8) + NT - 1) / NT; ++r) {
+      const int e = t + NT * r;
+      if (e < G * (kHeadDim / 8)) sh.q[e / (kHeadDim / 8)][e % (kHeadDim / 8)] = qv[r];
+    }
   }
   __syncthreads();
   BPC_STAMP(1, 6);
-  double xb = 0.0;  // the group sum of row t / 4 (every lane of the quad)
+  double xb[RP];  // the group sum of row (t + NT rr) / 4 (every lane of the quad)
   if (t < 4 * L) {  // whole wavefronts (4 L is a multiple of 64)
-    const int i = t >> 2, c = t & 3;
-    // four heads at a time: four independent fixed-order chains interleave;
-    // P is re-read from LDS eight coordinates at a time (held whole, as 32
-    // values, it would not fit beside the accumulators)
-    for (int g0 = 0; g0 < G; g0 += 4) {
-      double acc[4] = {0.0, 0.0, 0.0, 0.0};
+    double m = 0.0;
+#pragma unroll
+    for (int rr = 0; rr < RP; ++rr) {
+      xb[rr] = 0.0;
+      if (t + NT * rr >= 4 * L) continue;  // uniform over the wavefront
+      const int i = (t + NT * rr) >> 2, c = t & 3;
+      // four heads at a time: four independent fixed-order chains interleave;
+      // P is re-read from LDS eight coordinates at a time (held whole, as 32
+      // values, it would not fit beside the accumulators)
+      for (int g0 = 0; g0 < G; g0 += 4) {
+        double acc[4] = {0.0, 0.0, 0.0, 0.0};
 #pragma unroll 1
-      for (int j = 0; j < 4; ++j) {
-        const float4 pa = sh.P[i * 32 + c * 8 + ((2 * j) ^ qpack_swz(i, c))];
-        const float4 pb = sh.P[i * 32 + c * 8 + ((2 * j + 1) ^ qpack_swz(i, c))];
-        const float pf[8] = {pa.x, pa.y, pa.z, pa.w, pb.x, pb.y, pb.z, pb.w};
-        uint32_t w4[4][4];
-#pragma unroll
-        for (int hh = 0; hh < 4; ++hh) {
-          // coordinates 32 c + 8 j .. 32 c + 8 j + 7 of head g0 + hh (a head
-          // past G reads head g0, whose result is dropped)
-          const uint4 qq = sh.q[g0 + hh < G ? g0 + hh : g0][4 * c + j];
-          w4[hh][0] = qq.x, w4[hh][1] = qq.y, w4[hh][2] = qq.z, w4[hh][3] = qq.w;
-        }
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const double d0 = (double)pf[2 * e], d1 = (double)pf[2 * e + 1];
+        for (int j = 0; j < 4; ++j) {
+          const float4 pa = sh.P[i * 32 + c * 8 + ((2 * j) ^ qpack_swz(i, c))];
+          const float4 pb = sh.P[i * 32 + c * 8 + ((2 * j + 1) ^ qpack_swz(i, c))];
+          const float pf[8] = {pa.x, pa.y, pa.z, pa.w, pb.x, pb.y, pb.z, pb.w};
+          uint32_t w4[4][4];
 #pragma unroll
           for (int hh = 0; hh < 4; ++hh) {
-            acc[hh] = __builtin_fma(d0, (double)bf16_to_f32(w4[hh][e] & 0xFFFFu), acc[hh]);
-            acc[hh] = __builtin_fma(d1, (double)bf16_to_f32(w4[hh][e] >> 16), acc[hh]);
+            // coordinates 32 c + 8 j .. 32 c + 8 j + 7 of head g0 + hh (a head
+            // past G reads head g0, whose result is dropped)
+            const uint4 qq = sh.q[g0 + hh < G ? (g0 + hh) % GMAX : g0 % GMAX][4 * c + j];
+            w4[hh][0] = qq.x, w4[hh][1] = qq.y, w4[hh][2] = qq.z, w4[hh][3] = qq.w;
+          }
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const double d0 = (double)pf[2 * e], d1 = (double)pf[2 * e + 1];
+#pragma unroll
+            for (int hh = 0; hh < 4; ++hh) {
+              acc[hh] = __builtin_fma(d0, (double)bf16_to_f32(w4[hh][e] & 0xFFFFu), acc[hh]);
+              acc[hh] = __builtin_fma(d1, (double)bf16_to_f32(w4[hh][e] >> 16), acc[hh]);
+            }
           }
         }
-      }
 #pragma unroll
-      for (int hh = 0; hh < 4; ++hh) {
-        // ((b0 + b1) + (b2 + b3)) on every lane of the quad
-        const double s01 = dadd(acc[hh], dpp_f64<kDppQuadXor1>(acc[hh]));
-        const double a = dadd(s01, dpp_f64<kDppQuadXor2>(s01));
-        if (g0 + hh < G) xb = (g0 + hh == 0) ? a : dadd(xb, a);
+        for (int hh = 0; hh < 4; ++hh) {
+          // ((b0 + b1) + (b2 + b3)) on every lane of the quad
+          const double s01 = dadd(acc[hh], dpp_f64<kDppQuadXor1>(acc[hh]));
+          const double a = dadd(s01, dpp_f64<kDppQuadXor2>(s01));
+          if (g0 + hh < G) xb[rr] = (g0 + hh == 0) ? a : dadd(xb[rr], a);
+        }
       }
+      m = fmax(m, fabs(xb[rr]));
     }
     // max |xbar| of the wavefront: the quads are uniform, so two mirrors
     // give the maximum of 16 lanes, and four read-lanes that of the wavefront
-    double m = fabs(xb);
     m = fmax(m, dpp_f64<kDppHalfMirror>(m));
     m = fmax(m, dpp_f64<kDppMirror>(m));
     const int mlo = __double2loint(m), mhi = __double2hiint(m);
@@ -213,15 +231,19 @@ __device__ __forceinline__ void qpack_block(QpackShared<L>& sh, QpackOut<L>& o, 
   if (t < 4 * L) {
     double m = o.wmax[0];
 #pragma unroll
-    for (int w = 1; w < 4 * L / 64; ++w) m = fmax(m, o.wmax[w]);
-    const int p = (m > 0.0) ? (int)round(dmul(xb, 127.0) / m) : 0;
-    const uint32_t mag = (uint32_t)abs(p);
-    // every quad holds one row: each plane's ballot has its bits at lanes 4 k
+    for (int w = 1; w < ACTW; ++w) m = fmax(m, o.wmax[w]);
 #pragma unroll
-    for (int plane = 0; plane < 8; ++plane) {
-      const bool on = plane == 0 ? (p >= 0) : (((mag >> (plane - 1)) & 1u) != 0u);
-      const uint32_t piece = every_fourth_bit(__ballot(on));  // rows 16 wid .. 16 wid + 15
-      if (lane == 0) o.qc16[plane * (L / 16) + wid] = (uint16_t)piece;
+    for (int rr = 0; rr < RP; ++rr) {
+      if (t + NT * rr >= 4 * L) continue;
+      const int p = (m > 0.0) ? (int)round(dmul(xb[rr], 127.0) / m) : 0;
+      const uint32_t mag = (uint32_t)abs(p);
+      // every quad holds one row: each plane's ballot has its bits at lanes 4 k
+#pragma unroll
+      for (int plane = 0; plane < 8; ++plane) {
+        const bool on = plane == 0 ? (p >= 0) : (((mag >> (plane - 1)) & 1u) != 0u);
+        const uint32_t piece = every_fourth_bit(__ballot(on));  // rows 16 (wid + rr NT / 64) .. + 15
+        if (lane == 0) o.qc16[plane * (L / 16) + rr * (NT / 64) + wid] = (uint16_t)piece;
+      }
     }
   }
   __syncthreads();
@@ -337,8 +359,8 @@ __device__ __forceinline__ void score_body(ScoreShared<L>& sh, int bh, int s, co
   // (more loads in flight during it delay P for the workgroups dispatched
   // later on the CU, and the step gets slower).
   u32x4_t cw[RD];
-  qpack_block<L, NT>(sh.u.qp, sh.qo, q + ((size_t)b * Hkv * G + (size_t)h * G) * kHeadDim, P + b * sP_b + h * sP_h,
-                     G, [&]() { cw[0] = load_group(0); });
+  qpack_block<L, NT, kMaxGroup>(sh.u.qp, sh.qo, q + ((size_t)b * Hkv * G + (size_t)h * G) * kHeadDim,
+                                P + b * sP_b + h * sP_h, G, [&]() { cw[0] = load_group(0); });
   BPC_STAMP(1, 5);
   const uint32_t* qcw = reinterpret_cast<const uint32_t*>(sh.qo.qc16);
   uint32_t sg[W], M[7][W];
@@ -792,11 +814,23 @@ __device__ __forceinline__ void attend_pass(uint32_t rk, const uint32_t (&rv)[4]
   }
 }
 
+// Data one workgroup publishes for others of the same launch: agent-scope
+// atomic stores and loads (coherent across the XCDs' L2 caches without a
+// write-back of the L2), ordered by stores_complete() before the arrival.
+__device__ __forceinline__ void pub_store(uint32_t* p, uint32_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint32_t pub_load(const uint32_t* p) {
+  return __hip_atomic_load(const_cast<uint32_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// every store this thread has issued is complete before anything after it
+__device__ __forceinline__ void stores_complete() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
 // The workgroup's partial for each query head g: each wavefront reduces its
 // weighted V over its four row groups; the wavefronts are combined under
 // their common maximum into pb[g] = (max, sum, o[128]) (base-2 logits).
 // o_s and st_s are LDS arrays; the caller ensures o_s is free to write.
-template <int G>
+template <int G, bool PUBLISH = false>  // PUBLISH: agent-scope atomic stores (read by the merging workgroup)
 __device__ __forceinline__ void write_partial(float (&o_s)[kAttnWaves][G][kHeadDim], float (&st_s)[kAttnWaves][G][2],
                                               const float (&Mx)[G], const float (&Ls)[G], float (&o)[G][8],
                                               float* __restrict__ pb) {
@@ -840,7 +874,10 @@ __device__ __forceinline__ void write_partial(float (&o_s)[kAttnWaves][G][kHeadD
         acc = fmaf(d == 1 ? st_s[w][g][1] : o_s[w][g][d - 2], f, acc);
       }
     }
-    pb[e] = acc;
+    if constexpr (PUBLISH)
+      pub_store(reinterpret_cast<uint32_t*>(pb) + e, __float_as_uint(acc));
+    else
+      pb[e] = acc;
   }
 }
 
@@ -1388,6 +1425,821 @@ __global__ __launch_bounds__(kHeadDim) void merge_kernel(int Hkv, int G, int nch
   BPC_STAMP(3, 1);
 }
 
+// ===========================================================================
+// Fused decode step: the whole step in one launch, one 256-thread workgroup
+// per slice, every workgroup of the grid resident at once (the host checks
+// the occupancy).  A workgroup
+//  1. packs its (b, h)'s query group and scores its slice (64 keys per lane,
+//     distances kept in registers, an LDS histogram);
+//  2. publishes its window record, its histogram summary and its coarse
+//     prefix, then waits until every slice of (b, h) has published;
+//  3. derives T*, its tie quota and its output offset from the records (the
+//     one-round window rule of the attention kernel above; else the exact
+//     two rounds, the second publishing the fine bins of the coarse bin c*);
+//  4. selects its kept keys straight from its registers, in key order,
+//     gathers their K/V rows and accumulates its softmax partial;
+//  5. publishes the partial; the last workgroup of (b, h) to do so merges the
+//     partials of every slice into the output and returns the (b, h)'s
+//     arrival counters to zero for the next call.
+// Handoffs between workgroups use agent-scope atomic stores and loads for
+// the published data, a wait for the stores' completion, and a relaxed
+// agent-scope counter: the published data are visible to any workgroup once
+// the counter shows their writer's arrival, with no L2 write-back.  The only
+// wait is bounded; it is never reached when the grid is resident, and a
+// workgroup that reaches it keeps no rows.
+// ===========================================================================
+constexpr int kFusedThreads = 256;
+constexpr int kFusedWaves = kFusedThreads / 64;
+constexpr int kFusedRing = 8;              // 16-byte code loads in flight per thread
+constexpr unsigned kSpinLimit = 1u << 22;  // bounded wait on the arrival counter
+// published per slice: the window record, (kth, cmin, count, window end), the
+// coarse prefix (129 counts) and, in the exact two-round path, the counts of
+// the 128 fine bins of c*
+constexpr int kPubMeta = kWinRec;
+constexpr int kPubCoarse = kPubMeta + 4;
+constexpr int kPubFine = kPubCoarse + kCoarseStride;
+constexpr int kPubStride = kPubFine + (1 << kCoarseShift);
+static_assert(kPubStride == kFusedPubWords, "published record size");
+
+
+// Sum over the nslices slices of (b, h) of f(published word of slice u),
+// kBatch loads per thread in flight before the first is used.
+constexpr int kBatch = 8;
+template <class Addr, class F>
+__device__ __forceinline__ int sum_published(int nslices, Addr addr, F f) {
+  int acc = 0;
+  for (int u0 = 0; u0 < nslices; u0 += kBatch) {
+    uint32_t v[kBatch];
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) v[j] = pub_load(addr(min(u0 + j, nslices - 1)));
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) acc += (u0 + j < nslices) ? f(v[j]) : 0;
+  }
+  return acc;
+}
+// Copy nv published words, word e from src(e), to dst[e] in LDS; R loads per
+// thread are in flight before the first is used.
+template <int R, class Src>
+__device__ __forceinline__ void copy_published(uint32_t* dst, int nv, Src src) {
+  for (int e0 = 0; e0 < nv; e0 += R * kFusedThreads) {
+    uint32_t v[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      const int e = e0 + (int)threadIdx.x + r * kFusedThreads;
+      v[r] = (e < nv) ? pub_load(src(e)) : 0u;
+    }
+    // the values are taken here, so that the compiler cannot sink each load
+    // into the conditional store that uses it (and wait on them one by one)
+#pragma unroll
+    for (int r = 0; r < R; ++r) __asm__ volatile("" : "+v"(v[r]));
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      const int e = e0 + (int)threadIdx.x + r * kFusedThreads;
+      if (e < nv) dst[e] = v[r];
+    }
+  }
+}
+
+template <int L, int G>
+struct FusedShared {
+  static constexpr int NB = dist_bins(L);
+  static constexpr int NBP = (NB + 127) & ~127;
+  struct Attn {
+    uint32_t win[kWinSlices][kWinRec];  // window records of the (b, h)'s slices (one-round threshold)
+    int rows[kRowCache];                // the candidates (key << 16 | distance), then over them the
+                                        // first kRowCache selected keys in rank order
+    uint32_t sel[kSlice / 32];          // the safeguard: bitmap of the slice's keys the hash selection took
+  };
+  union alignas(16) U {
+    uint32_t hist[NBP];
+    QpackShared<L, G> qp;
+    Attn at;
+    float o[kFusedWaves][G][kHeadDim];
+  } u;
+  QpackOut<L> qo;
+  uint32_t coarse[kCoarseBins];
+  uint32_t cc[kCoarseBins + 1];
+  uint32_t fine[1 << kCoarseShift];  // counts of the fine bins of c* (two-round path)
+  int gsum[2][kCoarseBins];          // two-round path: sums over slices
+  int wcnt[kFusedWaves][2];          // per wavefront: keys below T*, ties at T*
+  int kth, cmin, that, flag;
+  int red[2][kFusedWaves];
+  int wave_tot[2][kFusedWaves];
+  float st[kFusedWaves][G][2];
+  alignas(16) float pl[kFusedWaves][G][16];
+  uint4 q[G][kHeadDim / 8];
+};
+
+// waves per SIMD the kernel is built for: four 256-thread workgroups per CU
+// (the 1024-slice grid of a batch of 16 x 8 heads x 128K keys resident) where
+// LDS allows it; L = 128 holds 64 KB of histogram, so two
+template <int L, int G>
+constexpr int fused_waves() { return L == 128 ? 2 : G <= 4 ? 4 : G == 8 ? 3 : 1; }
+
+template <int L, int G>
+__global__ __launch_bounds__(kFusedThreads) __attribute__((amdgpu_waves_per_eu(fused_waves<L, G>()))) void fused_decode_kernel(
+    const uint16_t* __restrict__ q, const float* __restrict__ P, int64_t sP_b, int64_t sP_h,
+    const uint32_t* __restrict__ codes, int64_t sC_b, int64_t sC_h, const uint16_t* __restrict__ K, int64_t sK_b,
+    int64_t sK_h, int64_t sK_n, const uint16_t* __restrict__ V, int64_t sV_b, int64_t sV_h, int64_t sV_n, int BH,
+    int Hkv, int N, int k, int nslices, float scale_log2, uint32_t* __restrict__ sync, uint32_t* __restrict__ pub,
+    float* __restrict__ part, int32_t* __restrict__ rows, float* __restrict__ out, int32_t* __restrict__ idx_out,
+    int32_t* __restrict__ score_out, uint32_t* __restrict__ qcode_out, const int32_t* __restrict__ serr, int64_t sS_b,
+    int64_t sS_h, int m, int32_t* __restrict__ added_out) {
+  constexpr int W = L / 32;
+  constexpr int NT = kFusedThreads;
+  constexpr int NW = kFusedWaves;
+  constexpr int NB = FusedShared<L, G>::NB;
+  constexpr int NBP = FusedShared<L, G>::NBP;
+  constexpr int PER = kSlice / NT;       // keys per thread
+  constexpr int KPL = 4 / W;             // keys per 16-byte load
+  constexpr int NLD = PER / KPL;         // loads per thread
+  constexpr int RD = kFusedRing < NLD ? kFusedRing : NLD;
+  constexpr int KPW = kSlice / NW;       // keys per wavefront: a contiguous run
+  constexpr int KSTEP = 64 * KPL;        // keys per load of the wavefront
+  __shared__ FusedShared<L, G> sh;
+
+  int bh, s;
+  slice_tile(blockIdx.x, BH, nslices, bh, s);
+  const int b = bh / Hkv, h = bh % Hkv;
+  const int n0 = s * kSlice;
+  const int cnt = min(kSlice, N - n0);
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const size_t sl = (size_t)bh * nslices + s;
+  uint32_t* my_pub = pub + sl * kPubStride;
+  const uint32_t* bh_pub = pub + (size_t)bh * nslices * kPubStride;
+  uint32_t* bh_sync = sync + (size_t)bh * kFusedSyncWords;
+  BPC_STAMP(1, 0);
+
+  // ---- 1. query packing and scoring -----------------------------------
+  const uint32_t* cb = codes + b * sC_b + h * sC_h + (int64_t)n0 * W;
+  const bool full = cnt == kSlice && (reinterpret_cast<uintptr_t>(cb) & 15u) == 0;
+  auto key_of = [&](int it, int u) -> int { return wid * KPW + it * KSTEP + lane * KPL + u; };
+  auto load_group = [&](int r) -> u32x4_t {
+    const int n = key_of(r, 0);
+    if (full)
+      return __builtin_nontemporal_load(
+          reinterpret_cast<const u32x4_t*>(reinterpret_cast<const char*>(cb) + (uint32_t)n * (4u * W)));
+    return load_code_group<W>(cb, n, cnt, (reinterpret_cast<uintptr_t>(cb) & 15u) == 0);
+  };
+  u32x4_t cw[RD];
+  qpack_block<L, NT, G>(sh.u.qp, sh.qo, q + ((size_t)b * Hkv * G + (size_t)h * G) * kHeadDim, P + b * sP_b + h * sP_h,
+                        G, [&]() { cw[0] = load_group(0); });
+  BPC_STAMP(1, 1);
+  const uint32_t* qcw = reinterpret_cast<const uint32_t*>(sh.qo.qc16);
+  uint32_t sg[W], M[7][W];
+  int T = 0;  // sum |p_i|
+#pragma unroll
+  for (int w = 0; w < W; ++w) {
+    sg[w] = __builtin_amdgcn_readfirstlane(qcw[w]);
+#pragma unroll
+    for (int j = 0; j < 7; ++j) {
+      M[j][w] = __builtin_amdgcn_readfirstlane(qcw[(1 + j) * W + w]);
+      T += __popc(M[j][w]) << j;
+    }
+  }
+#pragma unroll
+  for (int r = 1; r < RD; ++r) cw[r] = load_group(r);
+  if (s == 0 && qcode_out && threadIdx.x < 8 * W) qcode_out[(size_t)bh * 8 * W + threadIdx.x] = qcw[threadIdx.x];
+  for (int r = threadIdx.x; r < NBP; r += NT) sh.u.hist[r] = 0u;
+  __syncthreads();
+  // distances (< 2^14) two per register: key i = it * KPL + u is half i & 1 of dpk[i >> 1]
+  uint32_t dpk[PER / 2];
+#pragma unroll
+  for (int it = 0; it < NLD; ++it) {
+    const u32x4_t c = cw[it % RD];
+    if (it + RD < NLD) cw[it % RD] = load_group(it + RD);
+#pragma unroll
+    for (int u = 0; u < KPL; ++u) {
+      const bool valid = key_of(it, u) < cnt;
+      const uint32_t d = valid ? code_distance<W>(c, u, M, sg) : 0xFFFFu;
+      const int i = it * KPL + u;
+      dpk[i >> 1] = (i & 1) ? (dpk[i >> 1] | (d << 16)) : d;
+      if (i & 1) __asm__ volatile("" : "+v"(dpk[i >> 1]));
+      if (valid) atomicAdd(&sh.u.hist[d], 1u);
+    }
+  }
+  __syncthreads();
+  BPC_STAMP(1, 2);
+  auto dist_of = [&](int it, int u) -> int {
+    const int i = it * KPL + u;
+    return (int)((dpk[i >> 1] >> ((i & 1) << 4)) & 0xFFFFu);
+  };
+  if (score_out) {  // debug output
+    int32_t* so = score_out + (size_t)bh * N + n0;
+#pragma unroll
+    for (int it = 0; it < NLD; ++it)
+#pragma unroll
+      for (int u = 0; u < KPL; ++u) {
+        const int n = key_of(it, u);
+        if (n < cnt) so[n] = T - 2 * dist_of(it, u);
+      }
+  }
+
+  // ---- 2. histogram summary, published --------------------------------
+  // the histogram in prefix form per coarse bin (count in [128 (t >> 7), t))
+  // << 16 | count at t, and the coarse counts
+  for (int seg = threadIdx.x; seg < 1024; seg += NT) {
+    const int cbin = seg >> 3, part8 = seg & 7;
+    const int fb0 = (cbin << kCoarseShift) + part8 * 16;
+    uint32_t cntv[16];
+    if (fb0 < NBP) {
+      const uint4* hv = reinterpret_cast<const uint4*>(sh.u.hist + fb0);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const uint4 x = hv[r];
+        cntv[4 * r] = x.x, cntv[4 * r + 1] = x.y, cntv[4 * r + 2] = x.z, cntv[4 * r + 3] = x.w;
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < 16; ++e) cntv[e] = 0u;
+    }
+    int local = 0;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) local += (int)cntv[e];
+    const int incl = group8_inclusive_sum(local);
+    if (part8 == 7) sh.coarse[cbin] = (uint32_t)incl;
+    if (fb0 < NBP) {
+      uint32_t run = (uint32_t)(incl - local);
+      uint4* hv = reinterpret_cast<uint4*>(sh.u.hist + fb0);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        uint32_t v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          v[e] = (run << 16) | cntv[4 * r + e];
+          run += cntv[4 * r + e];
+        }
+        hv[r] = make_uint4(v[0], v[1], v[2], v[3]);
+      }
+    }
+  }
+  __syncthreads();
+  // wave 0: coarse prefix, the lowest occupied coarse bin, and the fine bins
+  // of the slice's k-th key and of its m-th key, m = ceil(k cnt / N) (its
+  // share of the budget, its own estimate of the threshold)
+  const int mloc = (int)(((int64_t)k * cnt + N - 1) / N);
+  if (threadIdx.x < 64) {
+    const uint32_t c0 = sh.coarse[2 * lane], c1 = sh.coarse[2 * lane + 1];
+    const int x = wave_inclusive_sum((int)(c0 + c1));
+    const int ex = x - (int)(c0 + c1);
+    sh.cc[2 * lane] = (uint32_t)ex;
+    sh.cc[2 * lane + 1] = (uint32_t)ex + c0;
+    if (lane == 63) sh.cc[kCoarseBins] = (uint32_t)x;
+    auto first_coarse = [&](int need) -> int {
+      const int f0 = first_lane(__ballot(ex + (int)c0 >= need)), f1 = first_lane(__ballot(x >= need));
+      return min(f0 < 64 ? 2 * f0 : 1 << 30, f1 < 64 ? 2 * f1 + 1 : 1 << 30);
+    };
+    const int cs = first_coarse(k), cs2 = first_coarse(mloc);
+    const int g0 = first_lane(__ballot(c0 != 0u)), g1 = first_lane(__ballot(c1 != 0u));
+    auto fine_first = [&](int c, int need) -> int {
+      if (c < 0 || c >= kCoarseBins) return NB - 1;
+      const int below = __builtin_amdgcn_readlane((c & 1) ? ex + (int)c0 : ex, c >> 1);
+      const int t0 = (c << kCoarseShift) + lane, t1 = t0 + 64;
+      const uint32_t v0 = (t0 < NBP) ? sh.u.hist[t0] : 0u, v1 = (t1 < NBP) ? sh.u.hist[t1] : 0u;
+      const unsigned long long r0 = __ballot(below + (int)(v0 >> 16) + (int)(v0 & 0xFFFFu) >= need);
+      const unsigned long long r1 = __ballot(below + (int)(v1 >> 16) + (int)(v1 & 0xFFFFu) >= need);
+      return r0 ? (c << kCoarseShift) + first_lane(r0) : r1 ? (c << kCoarseShift) + 64 + first_lane(r1) : NB - 1;
+    };
+    const int kth_w = fine_first((cnt >= k) ? cs : -1, k);
+    const int that_w = fine_first(cs2, mloc);
+    if (lane == 0) {
+      sh.kth = kth_w;
+      sh.that = that_w;
+      sh.cmin = min(g0 < 64 ? 2 * g0 : kCoarseBins - 1, g1 < 64 ? 2 * g1 + 1 : kCoarseBins - 1);
+    }
+  }
+  __syncthreads();
+  int cand_max;
+  {
+    // the window: kWinBins distances ending `up` above the slice's estimate t,
+    // `up` about six standard deviations of that estimate
+    auto cum = [&](int t) -> uint32_t {  // keys with distance <= t
+      if (t < 0) return 0u;
+      if (t >= NBP) return (uint32_t)cnt;
+      const uint32_t v = sh.u.hist[t];
+      return sh.cc[t >> kCoarseShift] + (v >> 16) + (v & 0xFFFFu);
+    };
+    const int that = sh.that;
+    const int dens17 = max((int)cum(that + 8) - (int)cum(that - 9), 1);
+    const int up = min(max((int)ceilf(6.0f * sqrtf((float)mloc) * 17.0f / (float)dens17), 4), kWinBins - 32);
+    const int wbase = max(that + up - (kWinBins - 1), 0);
+    // the largest distance on the candidate list: the window's end, at most
+    // the slice's k-th smallest distance (T* never exceeds the latter)
+    cand_max = min(wbase + kWinBins - 1, sh.kth);
+    if (threadIdx.x < kWinBins / 2)
+      pub_store(my_pub + 4 + threadIdx.x, cum(wbase + 2 * threadIdx.x) | (cum(wbase + 2 * threadIdx.x + 1) << 16));
+    else if (threadIdx.x < kWinBins / 2 + 4) {
+      const int j = threadIdx.x - kWinBins / 2;
+      const uint32_t hdr[4] = {(uint32_t)wbase, (uint32_t)cand_max, wbase > 0 ? cum(wbase - 1) : 0u,
+                               (uint32_t)cnt};
+      pub_store(my_pub + j, hdr[j]);
+    } else if (threadIdx.x < kWinBins / 2 + 8) {
+      const int j = threadIdx.x - kWinBins / 2 - 4;
+      const uint32_t mt[4] = {(uint32_t)sh.kth, (uint32_t)sh.cmin, (uint32_t)cnt, 0u};
+      pub_store(my_pub + kPubMeta + j, mt[j]);
+    }
+    for (int c = threadIdx.x; c <= kCoarseBins; c += NT) pub_store(my_pub + kPubCoarse + c, sh.cc[c]);
+  }
+  // arrival: every published store of the workgroup is complete first (and
+  // every read of the histogram, whose area holds the candidates next)
+  stores_complete();
+  __syncthreads();
+  if (threadIdx.x == 0) __hip_atomic_fetch_add(bh_sync + 0, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  // While the other slices finish: the candidates (distance <= cand_max) in
+  // key order into the LDS list (at most kRowCache of them).  In key order a
+  // lane's KPL keys of one load follow those of the lanes below it: each
+  // wavefront counts its own, then writes from a running offset.
+  int ncand;
+  {
+    int c = 0;
+#pragma unroll
+    for (int it = 0; it < NLD; ++it)
+#pragma unroll
+      for (int u = 0; u < KPL; ++u) c += dist_of(it, u) <= cand_max;
+    c = wave_inclusive_sum(c);
+    if (lane == 63) sh.wcnt[wid][0] = c;
+  }
+  // the write pass re-derives its flags instead of keeping 64 comparisons
+#pragma unroll
+  for (int i = 0; i < PER / 2; ++i) __asm__ volatile("" : "+v"(dpk[i]));
+  __syncthreads();
+  {
+    int base = 0;
+    ncand = 0;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      base += (w < wid) ? sh.wcnt[w][0] : 0;
+      ncand += sh.wcnt[w][0];
+    }
+    if (ncand <= kRowCache) {
+      uint32_t* cl = reinterpret_cast<uint32_t*>(sh.u.at.rows);
+      int kb = wid * KPW + lane * KPL;  // the lane's first key (opaque: nothing derived from it is precomputed)
+      __asm__ volatile("" : "+v"(kb));
+#pragma unroll
+      for (int it = 0; it < NLD; ++it) {
+        int pos = base;
+        bool f[KPL];
+#pragma unroll
+        for (int u = 0; u < KPL; ++u) {
+          f[u] = dist_of(it, u) <= cand_max;
+          const unsigned long long mk = __ballot(f[u]);
+          pos += (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(mk >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mk, 0u));
+          base += (int)__popcll(mk);
+        }
+#pragma unroll
+        for (int u = 0; u < KPL; ++u)
+          if (f[u]) cl[pos++] = ((uint32_t)(kb + it * KSTEP + u) << 16) | (uint32_t)dist_of(it, u);
+      }
+    }
+  }
+  if (threadIdx.x == 0) {
+    unsigned it = 0;    while (pub_load(bh_sync + 0) < (uint32_t)nslices && ++it < kSpinLimit) __builtin_amdgcn_s_sleep(2);
+    sh.flag = it < kSpinLimit;
+  }
+  // the group's queries for the attention (its own loads, behind the wait)
+  if (threadIdx.x < G * kHeadDim / 8) {
+    const uint4* qb = reinterpret_cast<const uint4*>(q + ((size_t)b * Hkv * G + (size_t)h * G) * kHeadDim);
+    sh.q[threadIdx.x / (kHeadDim / 8)][threadIdx.x % (kHeadDim / 8)] = qb[threadIdx.x];
+  }
+  __syncthreads();
+  BPC_STAMP(1, 3);
+  const bool arrived = sh.flag != 0;
+
+  // ---- 3. the threshold T*, this slice's tie quota and offset ---------
+  int tstar = 0, take = 0, off = 0, kept = 0;
+  bool planned = false, by_window = false;
+  if (arrived && nslices <= kWinSlices) {
+    // one round over the window records (see the attention kernel above)
+    const int nv = nslices * kWinRec;
+    auto src = [&](int e) { return bh_pub + (size_t)(e / kWinRec) * kPubStride + e % kWinRec; };
+    if (nv <= 2 * NT)
+      copy_published<2>(&sh.u.at.win[0][0], nv, src);
+    else if (nv <= 4 * NT)
+      copy_published<4>(&sh.u.at.win[0][0], nv, src);
+    else
+      copy_published<(kWinSlices * kWinRec + NT - 1) / NT>(&sh.u.at.win[0][0], nv, src);
+    __syncthreads();
+    auto cum = [&](int u, int t) -> int {  // base_u - 1 <= t < base_u + kWinBins
+      const int j = t - (int)sh.u.at.win[u][0];
+      const uint32_t w = sh.u.at.win[u][4 + (max(j, 0) >> 1)];
+      return (j < 0) ? (int)sh.u.at.win[u][2] : (int)((j & 1) ? (w >> 16) : (w & 0xFFFFu));
+    };
+    const int lo = wave_reduce_maxmin<true>(lane < nslices ? (int)sh.u.at.win[lane][0] : 0);
+    const int hi = wave_reduce_maxmin<false>(lane < nslices ? (int)sh.u.at.win[lane][1] : (1 << 30));
+    bool below = false, badt = false;
+    const int t = lo - 1 + (int)threadIdx.x;
+    if (lo <= hi && t <= hi) {
+      int St = 0;
+#pragma unroll 8
+      for (int u = 0; u < nslices; ++u) St += cum(u, t);
+      if (t == lo - 1)
+        badt = St >= k;
+      else
+        below = St < k;
+      if (t == hi && St < k) badt = true;
+    }
+    const unsigned long long mbelow = __ballot(below), mbad = __ballot(badt);
+    if (lane == 0) sh.red[0][wid] = (int)__popcll(mbelow), sh.red[1][wid] = mbad != 0ull;
+    __syncthreads();
+    int cntlow = 0, bad = lo > hi;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) cntlow += sh.red[0][w], bad |= sh.red[1][w];
+    if (!bad) {
+      tstar = lo + cntlow;
+      int bu = 0, tu = 0;
+      if (lane < nslices) {
+        bu = cum(lane, tstar - 1);
+        tu = cum(lane, tstar) - bu;
+      }
+      const int bi = wave_inclusive_sum(bu), ti = wave_inclusive_sum(tu);
+      const int below_all = __builtin_amdgcn_readlane(bi, 63);
+      const int below_before = __builtin_amdgcn_readlane(bi - bu, s), ties_before = __builtin_amdgcn_readlane(ti - tu, s);
+      const int bs = __builtin_amdgcn_readlane(bu, s), ts = __builtin_amdgcn_readlane(tu, s);
+      const int need = k - below_all;
+      take = max(0, min(ts, need - ties_before));
+      off = below_before + min(need, ties_before);
+      kept = bs + take;
+      planned = by_window = true;
+    }
+    __syncthreads();  // the window area is reused below
+  }
+  if (arrived && !planned) {
+    // Two exact rounds.  Round 1: the coarse bin c* of the k-th smallest
+    // distance from every slice's coarse prefix.
+    if (threadIdx.x < kCoarseBins) {
+      const int c = threadIdx.x;
+      const int gc = sum_published(nslices, [&](int u) { return bh_pub + (size_t)u * kPubStride + kPubCoarse + c + 1; },
+                                   [](uint32_t v) { return (int)v; });
+      sh.gsum[0][c] = gc;  // keys of all slices with coarse bin <= c
+      const unsigned long long mk = __ballot(gc >= k);
+      if (lane == 0) sh.red[0][wid] = mk ? first_lane(mk) + 64 * wid : (1 << 30);
+    }
+    __syncthreads();
+    const int cstar = min(min(sh.red[0][0], sh.red[0][1]), kCoarseBins - 1);
+    const int below_c = (cstar > 0) ? sh.gsum[0][cstar - 1] : 0;
+    // Round 2: this slice's fine bins of c*, counted from its registers and
+    // published in prefix form ((count below bin j in c*) << 16 | count at j)
+    for (int j = threadIdx.x; j < (1 << kCoarseShift); j += NT) sh.fine[j] = 0u;
+    __syncthreads();
+#pragma unroll
+    for (int it = 0; it < NLD; ++it)
+#pragma unroll
+      for (int u = 0; u < KPL; ++u) {
+        const int d = dist_of(it, u);
+        if ((d >> kCoarseShift) == cstar && d < NB) atomicAdd(&sh.fine[d & ((1 << kCoarseShift) - 1)], 1u);
+      }
+    __syncthreads();
+    if (threadIdx.x < 64) {
+      const uint32_t a0 = sh.fine[2 * lane], a1 = sh.fine[2 * lane + 1];
+      const int x = wave_inclusive_sum((int)(a0 + a1));
+      const uint32_t ex = (uint32_t)x - a0 - a1;
+      pub_store(my_pub + kPubFine + 2 * lane, (ex << 16) | a0);
+      pub_store(my_pub + kPubFine + 2 * lane + 1, ((ex + a0) << 16) | a1);
+    }
+    stores_complete();
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      __hip_atomic_fetch_add(bh_sync + 1, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      unsigned it = 0;
+      while (pub_load(bh_sync + 1) < (uint32_t)nslices && ++it < kSpinLimit) __builtin_amdgcn_s_sleep(2);
+      sh.flag = it < kSpinLimit;
+    }
+    __syncthreads();
+    if (sh.flag) {
+      // bin j of c*: keys of all slices below it (exc) and up to it (inc)
+      if (threadIdx.x < (1 << kCoarseShift)) {
+        const int j = threadIdx.x;
+        auto at = [&](int u) { return bh_pub + (size_t)u * kPubStride + kPubFine + j; };
+        const int exc = sum_published(nslices, at, [](uint32_t v) { return (int)(v >> 16); });
+        const int inc = exc + sum_published(nslices, at, [](uint32_t v) { return (int)(v & 0xFFFFu); });
+        sh.gsum[1][j] = exc;
+        const unsigned long long mk = __ballot(below_c + inc >= k);
+        if (lane == 0) sh.red[1][wid] = mk ? first_lane(mk) + 64 * wid : (1 << 30);
+      }
+      __syncthreads();
+      const int jt = min(min(sh.red[1][0], sh.red[1][1]), (1 << kCoarseShift) - 1);
+      tstar = min((cstar << kCoarseShift) + jt, NB - 1);
+      const int need = k - (below_c + sh.gsum[1][jt]);  // keys at T* to take, over all slices
+      // keys below T* and ties at T* of the slices before s (thread u for
+      // slice u), and of s itself
+      int bl = 0, ti = 0, my_below = 0, my_tie = 0;
+      for (int u = threadIdx.x; u <= s; u += NT) {
+        const uint32_t* pu = bh_pub + (size_t)u * kPubStride;
+        const uint32_t ccu = pub_load(pu + kPubCoarse + cstar), fu = pub_load(pu + kPubFine + jt);
+        const int below = (int)ccu + (int)(fu >> 16), tie = (int)(fu & 0xFFFFu);
+        if (u < s) {
+          bl += below, ti += tie;
+        } else {
+          my_below = below, my_tie = tie;
+        }
+      }
+      bl = wave_inclusive_sum(bl);
+      ti = wave_inclusive_sum(ti);
+      if (lane == 63) sh.wave_tot[0][wid] = bl, sh.wave_tot[1][wid] = ti;
+      if ((s % NT) == (int)threadIdx.x) sh.red[0][2] = my_below, sh.red[1][2] = my_tie;
+      __syncthreads();
+      int below_before = 0, ties_before = 0;
+#pragma unroll
+      for (int w = 0; w < NW; ++w) below_before += sh.wave_tot[0][w], ties_before += sh.wave_tot[1][w];
+      my_below = sh.red[0][2], my_tie = sh.red[1][2];
+      take = max(0, min(my_tie, need - ties_before));
+      off = below_before + min(need, ties_before);
+      kept = my_below + take;
+      planned = true;
+      __syncthreads();
+    }
+  }
+  if (!planned) kept = 0;  // a bounded wait ran out: this slice contributes nothing
+  kept = max(0, min(kept, k - off));
+  BPC_STAMP(1, 4);
+
+  // ---- 4. selection and attention -----------------------------------
+  // A kept key's rank among the slice's kept keys (key order) is (keys below
+  // T* before it) + min(ties at T* before it, take).  With the one-round
+  // threshold every key at or below T* is a candidate (T* <= cand_max), and
+  // the selection reads the candidate list only; otherwise the slice's keys
+  // are walked again from the registers.
+  if (m > 0)
+    for (int i = threadIdx.x; i < kSlice / 32; i += NT) sh.u.at.sel[i] = 0u;
+  int32_t* grow = rows + (size_t)bh * k;  // the (b, h)'s global row list (ranks past the LDS list)
+  const bool from_cands = by_window && ncand <= kRowCache;
+  if (from_cands) {
+    // batches of 4 NT candidates: their ranks from one block scan of the
+    // packed (ties << 16 | below) counts; the kept keys are written over the
+    // list itself (a kept candidate's rank never exceeds its position, and a
+    // batch is read before the scan's barrier)
+    uint32_t* cl = reinterpret_cast<uint32_t*>(sh.u.at.rows);
+    int nkept = 0, tie_seen = 0, sbuf = 0;
+    __syncthreads();  // the candidate list (and a cleared bitmap) visible to all
+    for (int base = 0; base < ncand; base += 4 * NT) {
+      const int nvalid = ncand - base - (int)threadIdx.x * 4;
+      uint32_t cv[4];
+      int nb = 0, nt = 0;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        cv[e] = (e < nvalid) ? cl[base + threadIdx.x * 4 + e] : 0xFFFFFFFFu;
+        const int d = (int)(cv[e] & 0xFFFFu);
+        nb += (e < nvalid) && d < tstar;
+        nt += (e < nvalid) && d == tstar;
+      }
+      int tot;
+      const int pre = block_exclusive_scan_bits<NT, 0x70007u>((nt << 16) | nb, sh.wave_tot, sbuf, tot);
+      sbuf ^= 1;
+      int tie_rank = tie_seen + (pre >> 16);
+      int rank = nkept + (pre & 0xFFFF) + max(0, min(tie_rank, take) - min(tie_seen, take));
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int d = (e < nvalid) ? (int)(cv[e] & 0xFFFFu) : (1 << 30);
+        bool keep = d < tstar;
+        if (d == tstar) {
+          keep = tie_rank < take;
+          ++tie_rank;
+        }
+        if (keep && rank < kept) {
+          const int kin = (int)(cv[e] >> 16);
+          sh.u.at.rows[rank] = n0 + kin;
+          if (idx_out) idx_out[(size_t)bh * k + off + rank] = n0 + kin;
+          if (m > 0) atomicOr(&sh.u.at.sel[kin >> 5], 1u << (kin & 31));
+        }
+        rank += keep;
+      }
+      nkept += (tot & 0xFFFF) + max(0, min(tie_seen + (tot >> 16), take) - min(tie_seen, take));
+      tie_seen += tot >> 16;
+    }
+  } else {
+    int nb = 0, nt = 0;
+#pragma unroll
+    for (int it = 0; it < NLD; ++it)
+#pragma unroll
+      for (int u = 0; u < KPL; ++u) {
+        const int d = dist_of(it, u);
+        nb += d < tstar;
+        nt += d == tstar;
+      }
+    nb = wave_inclusive_sum(nb);
+    nt = wave_inclusive_sum(nt);
+    if (lane == 63) sh.wcnt[wid][0] = nb, sh.wcnt[wid][1] = nt;
+    __syncthreads();
+  int wb0 = 0, wt0 = 0;  // keys below T* and ties at T* in the wavefronts before this one
+#pragma unroll
+  for (int w = 0; w < NW; ++w)
+    if (w < wid) wb0 += sh.wcnt[w][0], wt0 += sh.wcnt[w][1];
+  // The walk writes LDS only (global stores in its fully unrolled loop make
+  // the compiler spill): the rows of ranks [lo, lo + kRowCache) into the LDS
+  // list and the selection bitmap.  Windows past the first are walked first
+  // and copied out to the (b, h)'s global row list; the first stays in LDS.
+  const int nwin = max(1, (kept + kRowCache - 1) / kRowCache);
+  for (int wnd = nwin - 1; wnd >= 0; --wnd) {
+    const int lo = wnd * kRowCache;
+    int wb = wb0, wt = wt0;
+    // the lane's first key, opaque to the compiler: values derived from the
+    // keys are computed where they are used, not hoisted out of this loop
+    // for all 64 keys (which would spill)
+    int kb = wid * KPW + lane * KPL;
+    __asm__ volatile("" : "+v"(kb));
+#pragma unroll
+    for (int it = 0; it < NLD; ++it) {
+      // the keys of one load of the wavefront in ascending order are (lane,
+      // u): a lane's KPL keys follow the keys of the lanes below it
+      bool fb[KPL], ft[KPL];
+      int rb = wb, rt = wt, tb = 0, tt = 0;
+#pragma unroll
+      for (int u = 0; u < KPL; ++u) {
+        const int d = dist_of(it, u);
+        fb[u] = d < tstar;
+        ft[u] = d == tstar;
+        const unsigned long long mb = __ballot(fb[u]), mt = __ballot(ft[u]);
+        rb += (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(mb >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mb, 0u));
+        rt += (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(mt >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mt, 0u));
+        tb += (int)__popcll(mb);
+        tt += (int)__popcll(mt);
+      }
+      wb += tb;
+      wt += tt;
+      if (tb + tt == 0) continue;  // uniform over the wavefront
+#pragma unroll
+      for (int u = 0; u < KPL; ++u) {
+        const bool keep = fb[u] || (ft[u] && rt < take);
+        const int rank = rb + min(rt, take);
+        if (keep && rank < kept) {
+          const int kin = kb + it * KSTEP + u;
+          if (m > 0 && wnd == 0) atomicOr(&sh.u.at.sel[kin >> 5], 1u << (kin & 31));
+          if (rank >= lo && rank < lo + kRowCache) sh.u.at.rows[rank - lo] = n0 + kin;
+        }
+        rb += fb[u];
+        rt += ft[u];
+      }
+    }
+    __syncthreads();
+    if (wnd > 0) {
+      const int nr = min(kRowCache, kept - lo);
+      for (int r = threadIdx.x; r < nr; r += NT) {
+        const int key = sh.u.at.rows[r];
+        grow[off + lo + r] = key;
+        if (idx_out) idx_out[(size_t)bh * k + off + lo + r] = key;
+      }
+      __syncthreads();
+    }
+  }
+  if (idx_out)
+    for (int r = threadIdx.x; r < min(kept, kRowCache); r += NT) idx_out[(size_t)bh * k + off + r] = sh.u.at.rows[r];
+  }
+  __syncthreads();  // the kept rows and the selection bitmap are complete
+  int extra = 0;
+  if (m > 0) {
+    // S_err entries of this slice the hash selection did not take, in S_err
+    // order (ascending keys), ranked kept + (their position among them); the
+    // ones past the LDS list are found again from S_err when they are read
+    const int32_t* se = serr + b * sS_b + h * sS_h;
+    int sbuf = 0;
+    for (int base = 0; base < m; base += 4 * NT) {
+      int key[4], add[4], na = 0;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int j = base + 4 * (int)threadIdx.x + u;
+        key[u] = (j < m) ? se[j] : -1;
+        const int kin = key[u] - n0;
+        const bool here = key[u] >= n0 && kin < cnt;
+        add[u] = here && !((sh.u.at.sel[kin >> 5] >> (kin & 31)) & 1u);
+        if (added_out) {
+          const bool outside = j < m && (key[u] < 0 || key[u] >= N);
+          if (here || (outside && s == 0)) added_out[(size_t)bh * m + j] = add[u];
+        }
+        na += add[u];
+      }
+      int tot;
+      int pos = kept + extra + block_exclusive_scan_bits<NT, 0x7u>(na, sh.wave_tot, sbuf, tot);
+      sbuf ^= 1;
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (add[u]) {
+          if (pos < kRowCache) sh.u.at.rows[pos] = key[u];
+          ++pos;
+        }
+      extra += tot;
+    }
+    __syncthreads();
+  }
+  const int nrows = kept + extra;
+  float Mx[G], Ls[G], o[G][8];
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    Mx[g] = -INFINITY, Ls[g] = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o[g][e] = 0.f;
+  }
+  const char* Kh = reinterpret_cast<const char*>(K + b * sK_b + h * sK_h);
+  const char* Vh = reinterpret_cast<const char*>(V + b * sV_b + h * sV_h);
+  const uint32_t kstride = (uint32_t)sK_n * 2u, vstride = (uint32_t)sV_n * 2u;
+  BPC_STAMP(1, 8);
+  if (nrows <= kRowCache) {
+    for (int q0 = wid * kAttnRows; q0 < nrows; q0 += NW * kAttnRows) {
+      const int nr = min(kAttnRows, nrows - q0);
+      const int c16 = lane & 15, r4 = lane >> 4;
+      const int kc = sh.u.at.rows[q0 + c16];
+      const int4 v4 = *reinterpret_cast<const int4*>(sh.u.at.rows + q0 + 4 * r4);
+      const uint32_t rk = c16 < nr ? (uint32_t)kc : 0u;
+      uint32_t rv[4];
+      rv[0] = 4 * r4 + 0 < nr ? (uint32_t)v4.x : 0u;
+      rv[1] = 4 * r4 + 1 < nr ? (uint32_t)v4.y : 0u;
+      rv[2] = 4 * r4 + 2 < nr ? (uint32_t)v4.z : 0u;
+      rv[3] = 4 * r4 + 3 < nr ? (uint32_t)v4.w : 0u;
+      attend_pass<G>(rk, rv, nr, sh.q, sh.pl[wid], Kh, kstride, Vh, vstride, scale_log2, Mx, Ls, o);
+    }
+  } else {
+    // more rows than the LDS list holds: rank r >= kRowCache is at
+    // grow[off + r] (a kept key) or is an extra row of the safeguard (found
+    // again from the S_err order)
+    const int32_t* se = (m > 0) ? serr + b * sS_b + h * sS_h : nullptr;
+    int jlo = 0;  // S_err entries before this slice's keys (S_err is ascending)
+    if (m > 0) {
+      int c = 0;
+      for (int j = threadIdx.x; j < m; j += NT) c += se[j] < n0;
+      c = wave_inclusive_sum(c);
+      if (lane == 63) sh.red[0][wid] = c;
+      __syncthreads();
+#pragma unroll
+      for (int w = 0; w < NW; ++w) jlo += sh.red[0][w];
+      __syncthreads();
+    }
+    auto rank_row = [&](int r) -> uint32_t {
+      if (r >= nrows) return 0u;
+      if (r < kRowCache) return (uint32_t)sh.u.at.rows[r];
+      if (r < kept) return (uint32_t)grow[off + r];
+      // the (r - kept)-th added S_err entry of this slice: scan from jlo
+      int want = r - kept;
+      for (int j = jlo; j < m; ++j) {
+        const int key = se[j];
+        const int kin = key - n0;
+        if (key < n0 || kin >= cnt) break;
+        if (!((sh.u.at.sel[kin >> 5] >> (kin & 31)) & 1u) && want-- == 0) return (uint32_t)key;
+      }
+      return 0u;
+    };
+    for (int q0 = wid * kAttnRows; q0 < nrows; q0 += NW * kAttnRows) {
+      const int nr = min(kAttnRows, nrows - q0);
+      const int c16 = lane & 15, r4 = lane >> 4;
+      const uint32_t rk = c16 < nr ? rank_row(q0 + c16) : 0u;
+      uint32_t rv[4];
+#pragma unroll
+      for (int t = 0; t < 4; ++t) rv[t] = 4 * r4 + t < nr ? rank_row(q0 + 4 * r4 + t) : 0u;
+      attend_pass<G>(rk, rv, nr, sh.q, sh.pl[wid], Kh, kstride, Vh, vstride, scale_log2, Mx, Ls, o);
+    }
+  }
+  __syncthreads();  // the rows are read before the partial reuses their area
+  BPC_STAMP(1, 9);
+
+  // ---- 5. the partial, published; the last slice of (b, h) merges -----
+  float* my_part = part + sl * G * (kHeadDim + 2);
+  write_partial<G, true>(sh.u.o, sh.st, Mx, Ls, o, my_part);
+  stores_complete();
+  __syncthreads();
+  if (threadIdx.x == 0)
+    sh.flag = __hip_atomic_fetch_add(bh_sync + 2, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+              (uint32_t)(nslices - 1);
+  __syncthreads();
+  if (!sh.flag) return;
+  // the merge: every slice's (max, sum) per query head into LDS, then one
+  // output coordinate per thread and step
+  const float* pbh = part + (size_t)bh * nslices * G * (kHeadDim + 2);
+  const size_t cstride = (size_t)G * (kHeadDim + 2);
+  for (int e = threadIdx.x; e < G * kHeadDim; e += NT) {
+    const int g = e / kHeadDim, d = e % kHeadDim;
+    float Mg = -INFINITY, lsum = 0.f, acc = 0.f;
+    for (int u0 = 0; u0 < nslices; u0 += 8) {
+      float mt[8], lt[8], ot[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float* pc = pbh + (size_t)min(u0 + j, nslices - 1) * cstride + (size_t)g * (kHeadDim + 2);
+        mt[j] = __uint_as_float(pub_load(reinterpret_cast<const uint32_t*>(pc)));
+        lt[j] = __uint_as_float(pub_load(reinterpret_cast<const uint32_t*>(pc) + 1));
+        ot[j] = __uint_as_float(pub_load(reinterpret_cast<const uint32_t*>(pc) + 2 + d));
+      }
+      float mb = -INFINITY;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        if (u0 + j >= nslices) mt[j] = -INFINITY;
+        mb = fmaxf(mb, mt[j]);
+      }
+      const float Mn = fmaxf(Mg, mb);
+      if (Mn == -INFINITY) continue;
+      const float f = (Mg == -INFINITY) ? 0.f : exp2f(Mg - Mn);
+      lsum *= f, acc *= f;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float w = (mt[j] == -INFINITY) ? 0.f : exp2f(mt[j] - Mn);
+        lsum = fmaf(lt[j], w, lsum);
+        acc = fmaf(ot[j], w, acc);
+      }
+      Mg = Mn;
+    }
+    out[((size_t)b * Hkv * G + (size_t)h * G + g) * kHeadDim + d] = acc / lsum;
+  }
+  // every slice of (b, h) has passed both waits: the counters go back to zero
+  if (threadIdx.x < 3) __hip_atomic_store(bh_sync + threadIdx.x, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  BPC_STAMP(1, 10);
+}
+
 // ---------------------------------------------------------------------------
 // Launch sequence (all on the caller's stream): score (with the query
 // packing) -> attend -> merge.
@@ -1477,8 +2329,97 @@ hipError_t launch_dense(const DenseArgs& a) {
   return hipGetLastError();
 }
 
-hipError_t launch_decode(const DecodeArgs& a) {
-  const DecodeLayout lay = decode_layout(a.B, a.Hq, a.Hkv, a.N, a.L, a.k);
+// ---------------------------------------------------------------------------
+// The fused path: chosen when the grid fits on the device at once (the
+// occupancy of the kernel instance times the compute units), cached per
+// device, kernel instance and process.
+// ---------------------------------------------------------------------------
+static std::atomic<int> g_decode_path{0};
+void decode_set_path(int path) { g_decode_path.store(path); }
+
+template <int L, int G>
+static int fused_capacity() {
+  constexpr int kDevices = 64;
+  static std::atomic<int> cap[kDevices];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kDevices) return 0;
+  int c = cap[dev].load();
+  if (c == 0) {
+    int nb = 0, ncu = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, fused_decode_kernel<L, G>, kFusedThreads, 0) != hipSuccess ||
+        hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+      return 0;  // (the error is reported by the launch path)
+    c = max(nb * ncu, 0) + 1;  // stored + 1 so that 0 means "not queried"
+    cap[dev].store(c);
+  }
+  return c - 1;
+}
+
+template <int L>
+static int fused_capacity_L(int G) {
+  switch (G) {
+    case 1: return fused_capacity<L, 1>();
+    case 2: return fused_capacity<L, 2>();
+    case 4: return fused_capacity<L, 4>();
+    case 8: return fused_capacity<L, 8>();
+    case 16: return fused_capacity<L, 16>();
+    default: return 0;
+  }
+}
+
+bool decode_fused_ok(int B, int Hq, int Hkv, int N, int L) {
+  if (g_decode_path.load() == 1 || Hkv < 1 || Hq % Hkv || (int64_t)B * Hkv > kFusedMaxBH) return false;
+  const int G = Hq / Hkv;
+  const int64_t nwg = (int64_t)B * Hkv * ((N + kSlice - 1) / kSlice);
+  const int cap = L == 32 ? fused_capacity_L<32>(G) : L == 64 ? fused_capacity_L<64>(G) : fused_capacity_L<128>(G);
+  return nwg <= cap;
+}
+
+template <int L>
+static hipError_t launch_fused_L(const DecodeArgs& a, const DecodeLayout& lay) {
+  const int BH = a.B * a.Hkv;
+  const int nwg = BH * lay.nslices;
+  uint32_t* sync = reinterpret_cast<uint32_t*>(a.ws + lay.off_sync);
+  uint32_t* pub = reinterpret_cast<uint32_t*>(a.ws + lay.off_pub);
+  float* part = reinterpret_cast<float*>(a.ws + lay.off_part);
+  int32_t* rows = reinterpret_cast<int32_t*>(a.ws + lay.off_rows);
+  const float scale_log2 = a.sm_scale * 1.4426950408889634f;
+  hipStream_t st = a.stream;
+  auto mark = [&](int i) {
+    if (a.events) (void)hipEventRecord(a.events[i], st);
+  };
+  mark(0);
+  switch (lay.G) {
+#define BPC_FUSED_CASE(GG)                                                                                          \
+  case GG:                                                                                                          \
+    fused_decode_kernel<L, GG><<<nwg, kFusedThreads, 0, st>>>(                                                      \
+        a.q, a.P, a.sP_b, a.sP_h, a.codes, a.sC_b, a.sC_h, a.K, a.sK_b, a.sK_h, a.sK_n, a.V, a.sV_b, a.sV_h, a.sV_n, \
+        BH, a.Hkv, a.N, a.k, lay.nslices, scale_log2, sync, pub, part, rows, a.out, a.idx_out, a.score_out,          \
+        a.qcode_out, a.serr, a.sS_b, a.sS_h, a.m, a.added_out);                                                      \
+    break;
+    BPC_FUSED_CASE(1)
+    BPC_FUSED_CASE(2)
+    BPC_FUSED_CASE(4)
+    BPC_FUSED_CASE(8)
+    BPC_FUSED_CASE(16)
+#undef BPC_FUSED_CASE
+    default:
+      break;
+  }
+  mark(1);
+  mark(2);
+  mark(3);
+  return hipGetLastError();
+}
+
+hipError_t launch_decode(const DecodeArgs& a, const DecodeLayout& lay) {
+  if (lay.fused) {
+    switch (a.L) {
+      case 32: return launch_fused_L<32>(a, lay);
+      case 64: return launch_fused_L<64>(a, lay);
+      default: return launch_fused_L<128>(a, lay);
+    }
+  }
   switch (a.L) {
     case 32: return launch_decode_L<32>(a, lay);
     case 64: return launch_decode_L<64>(a, lay);

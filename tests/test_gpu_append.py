@@ -26,6 +26,16 @@ else:  # pragma: no cover
     bpc = None
 
 DEV = "cuda"
+
+@pytest.fixture(autouse=True, params=["fused", "three-launch"])
+def decode_path(request):
+    """Every test here runs on both decode paths: the single fused launch
+    (the default wherever the step's workgroups fit on the GPU at once) and
+    the three launches (the path for larger steps)."""
+    bpc.set_decode_path(0 if request.param == "fused" else 1)
+    yield request.param
+    bpc.set_decode_path(0)
+
 TOL = 2e-3
 
 

@@ -23,6 +23,16 @@ else:  # pragma: no cover - collected on CPU-only machines, never run
     bpc = None
 
 DEV = "cuda"
+
+@pytest.fixture(autouse=True, params=["fused", "three-launch"])
+def decode_path(request):
+    """Every test here runs on both decode paths: the single fused launch
+    (the default wherever the step's workgroups fit on the GPU at once) and
+    the three launches (the path for larger steps)."""
+    bpc.set_decode_path(0 if request.param == "fused" else 1)
+    yield request.param
+    bpc.set_decode_path(0)
+
 TOL = 2e-3
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "worked_example.json")
 
@@ -305,12 +315,15 @@ def test_decode_threshold_below_the_windows():
 
 
 def test_decode_garbage_workspace():
-    """The workspace needs no clearing: a first call on random bytes, and
-    later calls on the same workspace, all match the oracle."""
+    """Only the workspace's counter region (its first 256 KiB) needs zeroing
+    once: a first call on a workspace holding random bytes elsewhere, and
+    later calls on the same workspace, all match the oracle, on the fused
+    path and on the three-launch path."""
     rng = np.random.default_rng(21)
     q, K, V, codes, P = _random_case(rng, 2, 8, 2, 40000, 64, code_pool=30)
     B, Hq, Hkv, N, L, k = 2, 8, 2, 40000, 64, 800
     ws = torch.randint(0, 256, (bpc.decode_workspace_bytes(B, Hq, Hkv, N, L, k),), dtype=torch.uint8, device=DEV)
+    ws[:bpc.DECODE_ZEROED_BYTES] = 0
     cd = torch.from_numpy(codes.view(np.int32)).to(DEV)
     Pd = torch.from_numpy(P).to(DEV)
     outs = []
@@ -337,7 +350,7 @@ def test_decode_graph_replay():
     k = 600
     cd = torch.from_numpy(codes.view(np.int32)).to(DEV)
     Pd = torch.from_numpy(P).to(DEV)
-    ws = torch.empty(bpc.decode_workspace_bytes(2, 8, 2, 30000, 64, k), dtype=torch.uint8, device=DEV)
+    ws = torch.zeros(bpc.decode_workspace_bytes(2, 8, 2, 30000, 64, k), dtype=torch.uint8, device=DEV)
     out = torch.empty(2, 8, 128, dtype=torch.float32, device=DEV)
     eager = bpc.decode_attention(q, K, V, cd, Pd, k, out=torch.empty_like(out), workspace=ws).clone()
     torch.cuda.synchronize()
