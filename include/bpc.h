@@ -19,7 +19,9 @@
  * ---------------------------------------
  * - All tensor pointers are DEVICE pointers owned by the caller.  The
  *   library never allocates device memory; scratch space is passed in as a
- *   caller-owned workspace whose size the *_workspace_bytes functions give.
+ *   caller-owned workspace whose size the *_workspace_bytes functions give
+ *   (bpc_decode_attention_noalloc instead uses a static array the library
+ *   holds on each GPU, see there).
  * - bf16 tensors are passed as `const uint16_t*` bit patterns.
  * - Strides are in elements of the pointed-to type; the innermost
  *   dimension (D for K, V, q, P; the W code words of one key) is contiguous.
@@ -35,9 +37,10 @@
  *   Faults during kernel execution surface at the caller's next sync.
  * - Pointers must be 16-byte aligned and row strides multiples of 8
  *   elements (16 bytes), else BPC_EALIGN.
- * - Calls share no mutable state except a thread-local error message, so
- *   they are reentrant; two calls that share an output or a workspace must
- *   not overlap in time.
+ * - Calls share no mutable state except a thread-local error message (and,
+ *   for bpc_decode_attention_noalloc, that GPU's static scratch), so they
+ *   are reentrant; two calls that share an output or a workspace must not
+ *   overlap in time.
  * - Arithmetic that decides a code bit is IEEE binary64 in a fixed order:
  *   dot products over D split D into 4 consecutive blocks of D/4, sum each
  *   block in ascending order from +0 with separately rounded multiplies and
@@ -372,6 +375,42 @@ int bpc_decode_attention_profiled(const uint16_t* q,
                                   void* workspace, size_t workspace_bytes,
                                   void* stream,
                                   void* const* events, int n_events);
+
+/*
+ * bpc_decode_attention_noalloc -- bpc_decode_attention for callers that
+ * cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): the same computation and
+ * kernels, with the workspace taken from a static device array inside the
+ * library instead of a caller argument.  The call itself allocates nothing.
+ *
+ * Arguments, outputs and errors as for bpc_decode_attention, without the
+ * workspace arguments.  `stream` must belong to the current device.
+ * Limit: the decode workspace of the call (bpc_decode_workspace_bytes) must
+ * fit the array, bpc_decode_noalloc_max_bytes() = 64 MiB; a larger call
+ * returns BPC_EWORKSPACE and launches nothing.  (The fused single-launch
+ * path needs about 5 MiB at batch 16 x 8 KV heads x 131072 keys; the
+ * three-launch path, taken when a step's workgroups do not all fit on the
+ * GPU at once, needs about 100 KiB per 16384-key slice, so 64 MiB covers
+ * about 640 slices of it.)
+ * Each GPU holds one such array for the life of the process, and every call
+ * on that GPU uses it: two calls on one GPU that overlap in time (different
+ * streams without ordering, different host threads) race on it and give
+ * undefined results.  Calls ordered on one stream are safe.  Nothing in the
+ * array has to hold a particular value when a call starts.
+ */
+size_t bpc_decode_noalloc_max_bytes(void);
+int bpc_decode_attention_noalloc(const uint16_t* q,
+                                 const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t sK_n,
+                                 const uint16_t* V, int64_t sV_b, int64_t sV_h, int64_t sV_n,
+                                 const uint32_t* codes, int64_t sC_b, int64_t sC_h,
+                                 const float* P, int64_t sP_b, int64_t sP_h,
+                                 int B, int Hq, int Hkv, int N, int D, int L, int k,
+                                 float sm_scale,
+                                 float* out,
+                                 int32_t* idx_out,
+                                 int32_t* score_out,
+                                 uint32_t* qcode_out,
+                                 void* stream);
 
 #ifdef __cplusplus
 }

@@ -26,6 +26,8 @@ __all__ = [
     "decode_attention",
     "decode_workspace_bytes",
     "decode_attention_per_head",
+    "decode_attention_noalloc",
+    "decode_noalloc_max_bytes",
     "decode_per_head_workspace_bytes",
     "dense_attention",
     "select_hard",
@@ -84,6 +86,10 @@ _lib.bpc_select_hard.restype = _i
 _lib.bpc_select_hard.argtypes = [_p, _i64, _i64, _i, _i, _i, _i, _p, _p]
 _lib.bpc_set_decode_path.restype = _i
 _lib.bpc_set_decode_path.argtypes = [_i]
+_lib.bpc_decode_noalloc_max_bytes.restype = _sz
+_lib.bpc_decode_noalloc_max_bytes.argtypes = []
+_lib.bpc_decode_attention_noalloc.restype = _i
+_lib.bpc_decode_attention_noalloc.argtypes = _DECODE_ARGS[:-3] + [_p]
 _lib.bpc_decode_attention_profiled.restype = _i
 _lib.bpc_decode_attention_profiled.argtypes = _DECODE_ARGS + [ctypes.POINTER(_p), _i]
 
@@ -408,6 +414,37 @@ def decode_attention(q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, codes: t
                 ev.record(st)
             handles[i] = ev.cuda_event
         _check(_lib.bpc_decode_attention_profiled(*args, handles, len(events)), "bpc_decode_attention_profiled")
+    return out
+
+
+def decode_noalloc_max_bytes() -> int:
+    """Size of the library's static decode scratch (the limit of
+    decode_attention_noalloc)."""
+    return int(_lib.bpc_decode_noalloc_max_bytes())
+
+
+def decode_attention_noalloc(q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, codes: torch.Tensor,
+                             P: torch.Tensor, k: int, out: torch.Tensor, sm_scale: Optional[float] = None,
+                             N: Optional[int] = None, *, idx_out: Optional[torch.Tensor] = None,
+                             score_out: Optional[torch.Tensor] = None, qcode_out: Optional[torch.Tensor] = None,
+                             stream=None) -> torch.Tensor:
+    """decode_attention with the library's static scratch as the workspace:
+    the call allocates no device memory (the caller passes `out`).  Calls on
+    one GPU share the scratch, so calls that overlap in time race."""
+    B, Hq, Hkv, D, N, L, sPb, sPh = _decode_inputs(q, K, V, codes, P, k, N)
+    if out is None:
+        raise ValueError("out is required (the call allocates nothing)")
+    _exact_out(out, "out", torch.float32, (B, Hq, D))
+    _exact_out(idx_out, "idx_out", torch.int32, (B, Hkv, k))
+    _exact_out(score_out, "score_out", torch.int32, (B, Hkv, N))
+    _exact_out(qcode_out, "qcode_out", torch.int32, (B, Hkv, 8, L // 32))
+    _on_gpu(q, K, V, codes, P, out, idx_out, score_out, qcode_out)
+    if sm_scale is None:
+        sm_scale = 1.0 / math.sqrt(D)
+    _check(_lib.bpc_decode_attention_noalloc(
+        _ptr(q), _ptr(K), *_kv_strides(K), _ptr(V), *_kv_strides(V), _ptr(codes), codes.stride(0), codes.stride(1),
+        _ptr(P), sPb, sPh, B, Hq, Hkv, N, D, L, k, float(sm_scale), _ptr(out), _ptr(idx_out), _ptr(score_out),
+        _ptr(qcode_out), _stream(stream)), "bpc_decode_attention_noalloc")
     return out
 
 

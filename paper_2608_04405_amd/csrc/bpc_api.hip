@@ -7,6 +7,8 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <mutex>
+
 #include "bpc_internal.h"
 
 namespace bpc {
@@ -447,6 +449,62 @@ int bpc_select_hard(const float* err, int64_t sE_b, int64_t sE_h, int B, int Hkv
   hipError_t e = launch_select_hard(err, sE_b, sE_h, B, Hkv, N, m, serr_out, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "bpc_select_hard launch");
   return BPC_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Decode without a caller workspace: the workspace is `scratch`, a static
+// device array of kScratchBytes that every GPU the library runs on holds
+// until the process ends.  In host code `scratch` only names the symbol; its
+// device address on the current GPU comes from hipGetSymbolAddress, once per
+// device, and only that address is ever passed to kernels.
+// ---------------------------------------------------------------------------
+constexpr size_t kScratchBytes = size_t(64) << 20;
+constexpr int kScratchDevices = 64;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+static std::mutex g_scratch_mu;
+static void* g_scratch_ptr[kScratchDevices];
+
+// The scratch address on the GPU of `stream` (which must be the current
+// device); looked up on the first call on that device.
+static int scratch_for(void* stream, void** ptr) {
+  int dev = -1, sdev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  e = hipStreamGetDevice(static_cast<hipStream_t>(stream), &sdev);
+  if (e != hipSuccess) return hip_fail(e, "hipStreamGetDevice");
+  if (sdev != dev) return fail(BPC_EINVAL, "the stream belongs to device %d, the current device is %d", sdev, dev);
+  if (dev < 0 || dev >= kScratchDevices) return fail(BPC_EUNSUPPORTED, "device %d: at most %d devices", dev, kScratchDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (!p) return fail(BPC_EHIP, "hipGetSymbolAddress(scratch) returned NULL");
+    g_scratch_ptr[dev] = p;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return BPC_OK;
+}
+
+size_t bpc_decode_noalloc_max_bytes(void) { return kScratchBytes; }
+
+int bpc_decode_attention_noalloc(const uint16_t* q, const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t sK_n,
+                                 const uint16_t* V, int64_t sV_b, int64_t sV_h, int64_t sV_n,
+                                 const uint32_t* codes, int64_t sC_b, int64_t sC_h, const float* P, int64_t sP_b,
+                                 int64_t sP_h, int B, int Hq, int Hkv, int N, int D, int L, int k, float sm_scale,
+                                 float* out, int32_t* idx_out, int32_t* score_out, uint32_t* qcode_out,
+                                 void* stream) {
+  g_last_error[0] = 0;
+  const size_t need = bpc_decode_workspace_bytes(B, Hq, Hkv, N, D, L, k);
+  if (need > kScratchBytes)
+    return fail(BPC_EWORKSPACE, "this decode needs %zu bytes of scratch; the static scratch holds %zu (%zu MiB)",
+                need, kScratchBytes, kScratchBytes >> 20);
+  void* ws = nullptr;
+  int st = scratch_for(stream, &ws);
+  if (st) return st;
+  return decode_impl(q, K, sK_b, sK_h, sK_n, V, sV_b, sV_h, sV_n, codes, sC_b, sC_h, P, sP_b, sP_h, B, Hq, Hkv,
+                     N, D, L, k, sm_scale, out, idx_out, score_out, qcode_out, nullptr, 0, 0, 0, nullptr, ws,
+                     kScratchBytes, stream, nullptr, 0);
 }
 
 int bpc_decode_attention_profiled(const uint16_t* q, const uint16_t* K, int64_t sK_b, int64_t sK_h,
