@@ -1620,6 +1620,12 @@ __global__ __launch_bounds__(kFusedThreads) __attribute__((amdgpu_waves_per_eu(f
   }
   __syncthreads();
   BPC_STAMP(1, 2);
+  // The bookkeeping from here to the selection (histogram summary, the
+  // candidate list, the threshold) runs at raised wave priority: the
+  // workgroups still in it are the youngest on their CU, whose instructions
+  // otherwise queue behind the older workgroups' attention passes.  The
+  // attention itself runs at the normal priority.
+  __builtin_amdgcn_s_setprio(3);
   auto dist_of = [&](int it, int u) -> int {
     const int i = it * KPL + u;
     return (int)((dpk[i >> 1] >> ((i & 1) << 4)) & 0xFFFFu);
@@ -2132,6 +2138,7 @@ __global__ __launch_bounds__(kFusedThreads) __attribute__((amdgpu_waves_per_eu(f
   const char* Vh = reinterpret_cast<const char*>(V + b * sV_b + h * sV_h);
   const uint32_t kstride = (uint32_t)sK_n * 2u, vstride = (uint32_t)sV_n * 2u;
   BPC_STAMP(1, 8);
+  __builtin_amdgcn_s_setprio(0);
   if (nrows <= kRowCache) {
     for (int q0 = wid * kAttnRows; q0 < nrows; q0 += NW * kAttnRows) {
       const int nr = min(kAttnRows, nrows - q0);
