@@ -20,6 +20,7 @@ from __future__ import annotations
 
 import argparse
 import hashlib
+import numpy as np
 import json
 import math
 import os
@@ -40,10 +41,11 @@ def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=300)
     ap.add_argument("--instances", type=int, default=4)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-prefill", action="store_true")
+    ap.add_argument("--no-configs", action="store_true", help="measure only batch16_128k (skip the other workloads)")
     ap.add_argument("--decode-only", action="store_true",
                     help="skip the context measurements after the timed region (safeguard, fixed budgets, per "
                          "query head, dense, offline calibration), so that a profile holds only the decode step")
@@ -164,6 +166,132 @@ def summarize(roots, pmc_json=None) -> None:
         print(f"wrote {pmc_json}")
 
 
+def host_info():
+    """CPU model and the cores this process may use (the CPU baseline's host)."""
+    model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {"cpu_model": model, "usable_cores": len(os.sched_getaffinity(0))}
+
+
+def step_bytes(B, Hq, Hkv, N, D, L, k, layers=1):
+    """Algorithmic bytes of a decode step: codes read, gathered K+V rows, P,
+    q read and out written (scores and selections are not counted)."""
+    BH = B * Hkv
+    return layers * (BH * N * (L // 8) + BH * k * 2 * D * 2 + BH * L * D * 4 + B * Hq * D * (2 + 4))
+
+
+def time_steps(fn, steps, warmup, runs=1):
+    """Mean us per step of `runs` timed regions of `steps` calls each, after
+    `warmup` untimed calls; every region is bracketed by synchronizations."""
+    import torch
+    for j in range(warmup):
+        fn(j)
+    torch.cuda.synchronize()
+    res = []
+    for r in range(runs):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for j in range(steps):
+            fn(j)
+        e1.record()
+        torch.cuda.synchronize()
+        res.append(e0.elapsed_time(e1) / steps * 1e3)
+    return res
+
+
+def measure_config(bpc, cfg, dev, n_inst, steps, warmup, log_name):
+    """One workload end to end: inputs generated on the GPU, the prefill
+    (Algorithm 1 build with its fragile count, Algorithm 2 hashing of every
+    key), then the decode step timed.  A step is one decode of every layer
+    (the 32 layers of the stack one after another); single-layer workloads
+    rotate `n_inst` independent instances so that steps do not share data
+    through the 256 MB last-level cache."""
+    import torch
+    from workloads import make_layer
+    B, Hq, Hkv, D, N, L, k = cfg.B, cfg.Hq, cfg.Hkv, cfg.D, cfg.N, cfg.L, cfg.k
+    sm = 1.0 / math.sqrt(D)
+    layers = cfg.layers
+    n_data = layers if layers > 1 else n_inst
+    frag = torch.zeros(1, dtype=torch.int64, device=dev)
+    ws_build = torch.empty(bpc.build_workspace_bytes(B, Hkv, N, L), dtype=torch.uint8, device=dev)
+    build_ms = hash_ms = 0.0
+    data = []
+    t0 = time.time()
+    for i in range(n_data):
+        d = make_layer(cfg, layer=i, device=dev)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        ev[0].record()
+        P, codes, _ = bpc.build_hash(d["K"], d["G"].to(dev), fragile=frag if i == 0 or layers > 1 else None,
+                                     workspace=ws_build)
+        ev[1].record()
+        if i == 0 or layers > 1:
+            c2, _ = bpc.hash_keys(d["K"], P)
+        ev[2].record()
+        torch.cuda.synchronize()
+        if i == 0 or layers > 1:
+            build_ms += ev[0].elapsed_time(ev[1])
+            hash_ms += ev[1].elapsed_time(ev[2])
+            del c2
+        data.append({"q": d["q"], "K": d["K"], "V": d["V"], "codes": codes, "P": P})
+        del d
+    del ws_build
+    torch.cuda.empty_cache()
+    keys_pf = B * Hkv * N * (layers if layers > 1 else 1)
+    log(f"{log_name}: {n_data} layers/instances generated and built in {time.time() - t0:.1f}s")
+    ws = torch.zeros(bpc.decode_workspace_bytes(B, Hq, Hkv, N, L, k), dtype=torch.uint8, device=dev)
+    outs = [torch.empty(B, Hq, D, dtype=torch.float32, device=dev) for _ in range(min(n_data, 4))]
+
+    def step(j):
+        if layers > 1:  # every layer of the stack in turn
+            for i, it in enumerate(data):
+                bpc.decode_attention(it["q"], it["K"], it["V"], it["codes"], it["P"], k, sm, out=outs[i % 4],
+                                     workspace=ws)
+        else:
+            it = data[j % len(data)]
+            bpc.decode_attention(it["q"], it["K"], it["V"], it["codes"], it["P"], k, sm, out=outs[j % len(outs)],
+                                 workspace=ws)
+
+    runs = time_steps(step, steps, warmup, runs=3)
+    us = float(np.median(runs))
+    nbytes = step_bytes(B, Hq, Hkv, N, D, L, k, layers)
+    keys = B * Hkv * N * layers
+    res = {"workload": cfg.name, "B": B, "Hq": Hq, "Hkv": Hkv, "N": N, "L": L, "k": k, "layers": layers,
+           "us_per_step": round(us, 2), "runs_us_per_step": [round(x, 2) for x in runs],
+           "mean_us_per_step": round(float(np.mean(runs)), 2),
+           "keys_per_s": keys / (us * 1e-6), "token_positions_per_s": B * N * layers / (us * 1e-6),
+           "step_algorithmic_bytes": nbytes, "hbm_frac": round(nbytes / (us * 1e-6) / (HBM_PEAK_GBS * 1e9), 4),
+           "decode_path": "fused single launch" if bpc.decode_path_taken(B, Hq, Hkv, N, L) == 0 else "three launches",
+           "prefill": {"build_ms": round(build_ms, 2), "hash_ms": round(hash_ms, 2),
+                       "build_keys_per_s": keys_pf / (build_ms * 1e-3), "hash_keys_per_s": keys_pf / (hash_ms * 1e-3),
+                       "fragile_sign_decisions": int(frag.item()),
+                       "covers": "all layers" if layers > 1 else "one instance"}}
+    log(f"{log_name}: {res['us_per_step']} us/step, {res['keys_per_s']:.3g} keys/s, {res['hbm_frac'] * 100:.1f} % of "
+        f"8 TB/s; prefill {res['prefill']}")
+    del data, ws, outs
+    torch.cuda.empty_cache()
+    return res
+
+
+def copy_ceiling(dev):
+    """A plain 1 GiB device-to-device copy (read + write), the reference
+    rate of a streaming kernel on this GPU."""
+    import torch
+    src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    us = time_steps(lambda j: dst.copy_(src), 10, 3)[0]
+    del src, dst
+    torch.cuda.empty_cache()
+    return {"bytes_per_copy": 2 << 30, "us": round(us, 1), "GBps": round((2 << 30) / (us * 1e-6) / 1e9, 1),
+            "what": "torch copy of 1 GiB (1 GiB read + 1 GiB written), mean of 10"}
+
+
 def main():
     args = parse()
     if args.summarize:
@@ -174,7 +302,6 @@ def main():
               "(sequence, KV head) is independent; see DESIGN.md for how it would shard).", file=sys.stderr)
         sys.exit(2)
 
-    import numpy as np
     import torch
 
     import paper_2608_04405_amd as bpc
@@ -186,6 +313,7 @@ def main():
     B, Hq, Hkv, D, N, L, k = cfg.B, cfg.Hq, cfg.Hkv, cfg.D, cfg.N, cfg.L, cfg.k
     sm = 1.0 / math.sqrt(D)
     W = L // 32
+    host = host_info()
 
     # ---------------------------------------------------------------- inputs
     insts = []
@@ -200,14 +328,17 @@ def main():
     # ---------------------------------------------------------------- prefill
     ws_build = torch.empty(bpc.build_workspace_bytes(B, Hkv, N, L), dtype=torch.uint8, device=dev)
     prefill = {}
+    frag = torch.zeros(1, dtype=torch.int64, device=dev)
+    frag2 = torch.zeros(1, dtype=torch.int64, device=dev)
     for i, it in enumerate(insts):
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
         ev[0].record()
         err = torch.empty(B, Hkv, N, dtype=torch.float32, device=dev)
-        P, codes, _ = bpc.build_hash(it["K"], it["G"], err_out=err, workspace=ws_build)
+        P, codes, _ = bpc.build_hash(it["K"], it["G"], err_out=err, fragile=frag if i == 0 else None,
+                                     workspace=ws_build)
         ev[1].record()
         if i == 0 and not args.no_prefill:
-            codes2, _ = bpc.hash_keys(it["K"], P)
+            codes2, _ = bpc.hash_keys(it["K"], P, fragile=frag2)
         ev[2].record()
         torch.cuda.synchronize()
         it["P"], it["codes"], it["err"] = P, codes, err
@@ -217,8 +348,10 @@ def main():
             keys = B * Hkv * N
             prefill = {"build_ms": round(build_ms, 3), "hash_ms": round(hash_ms, 3),
                        "build_keys_per_s": keys / (build_ms / 1e3), "hash_keys_per_s": keys / (hash_ms / 1e3),
+                       "fragile_sign_decisions_build": int(frag.item()),
+                       "fragile_sign_decisions_hash": int(frag2.item()),
                        "what": "Algorithm 1 (build P and codes) and Algorithm 2 (hash every key) for the whole "
-                               "batch, fp64 fixed-order arithmetic"}
+                               "batch, fp64 fixed-order arithmetic; fragile = sign decisions with |a| < 1e-6"}
             del codes2
     del ws_build
     torch.cuda.empty_cache()
@@ -256,21 +389,39 @@ def main():
     keys_per_step = B * Hkv * N
     value = keys_per_step / (ms_per_step / 1e3)
     log(f"{ms_per_step * 1e3:.1f} us/step, {value:.4g} keys/s (wall {wall:.3f}s)")
+    # two more timed regions of the same length: three runs, median and mean
+    runs = [ms_per_step * 1e3] + time_steps(step, args.steps, 0, runs=2)
+    log(f"three runs: {[round(x, 2) for x in runs]} us/step")
 
     # ---------------------------------------------------------------- stage breakdown (same steps, with events)
     nst = bpc.DECODE_STAGES
-    stage_ms = np.zeros(nst)
     prof_steps = max(10, min(args.steps, 100))
-    evsets = [[torch.cuda.Event(enable_timing=True) for _ in range(nst + 1)] for _ in range(prof_steps)]
-    for j in range(prof_steps):
-        step(j, events=evsets[j])
-    torch.cuda.synchronize()
-    for evs in evsets:
-        for s in range(nst):
-            stage_ms[s] += evs[s].elapsed_time(evs[s + 1])
-    stage_ms /= prof_steps
-    stages = {n: round(float(t) * 1e3, 2) for n, t in zip(bpc.DECODE_STAGE_NAMES, stage_ms)}  # microseconds
-    log(f"stages (us): {stages}")
+
+    def stage_times():
+        t = np.zeros(nst)
+        evsets = [[torch.cuda.Event(enable_timing=True) for _ in range(nst + 1)] for _ in range(prof_steps)]
+        for j in range(prof_steps):
+            step(j, events=evsets[j])
+        torch.cuda.synchronize()
+        for evs in evsets:
+            for s in range(nst):
+                t[s] += evs[s].elapsed_time(evs[s + 1])
+        return {n: round(float(x) / prof_steps * 1e3, 2) for n, x in zip(bpc.DECODE_STAGE_NAMES, t)}
+
+    fused = bpc.decode_path_taken(B, Hq, Hkv, N, L) == 0
+    stages = stage_times()  # on the fused path the whole step is the first stage (one launch)
+    bpc.set_decode_path(1)
+    ws3 = torch.zeros(bpc.decode_workspace_bytes(B, Hq, Hkv, N, L, k), dtype=torch.uint8, device=dev)
+    ws_keep, ws = ws, ws3
+    for j in range(args.warmup):
+        step(j)
+    three = stage_times()
+    three_us = time_steps(step, prof_steps, 0)[0]
+    ws = ws_keep
+    del ws3
+    torch.cuda.empty_cache()
+    bpc.set_decode_path(0 if args.decode_path == "auto" else 1)
+    log(f"stages (us): {stages}; three-launch path: {three}, {three_us:.1f} us/step")
 
     eas, fixed, per_head, dense, opc = {}, {}, {}, {}, {}
     if not args.decode_only:
@@ -287,36 +438,19 @@ def main():
         ev[1].record()
         torch.cuda.synchronize()
         select_ms = ev[0].elapsed_time(ev[1]) / len(insts)
-        for j in range(args.warmup):
+
+        def eas_step(j):
             it = insts[j % len(insts)]
             bpc.decode_attention(it["q"], it["K"], it["V"], it["codes"], it["P"], k_hash, sm, out=outs[j % len(insts)],
                                  serr=it["serr"], workspace=ws)
-        eas_steps = max(10, min(args.steps, 100))
-        ev[0].record()
-        for j in range(eas_steps):
-            it = insts[j % len(insts)]
-            bpc.decode_attention(it["q"], it["K"], it["V"], it["codes"], it["P"], k_hash, sm, out=outs[j % len(insts)],
-                                 serr=it["serr"], workspace=ws)
-        ev[1].record()
-        torch.cuda.synchronize()
-        eas = {"us_per_step": round(ev[0].elapsed_time(ev[1]) / eas_steps * 1e3, 2), "k_hash": k_hash, "m": m_eas,
-               "select_hard_ms": round(select_ms, 3),
+
+        eas = {"us_per_step": round(time_steps(eas_step, prof_steps, args.warmup)[0], 2), "k_hash": k_hash,
+               "m": m_eas, "select_hard_ms": round(select_ms, 3),
                "what": "decode step over S_hash (top-2359 by hash score) united with S_err (263 keys of largest "
                        "reconstruction error, chosen per (b, h) at prefill by select_hard)"}
         log(f"safeguard: {eas}")
 
         # ---------------------------------------------------------------- fixed-count budgets (context)
-        # the same step with k = 1024 and k = 2048 keys instead of 2 % of N
-        def timed(fn, nsteps):
-            for j in range(args.warmup):
-                fn(j)
-            ev[0].record()
-            for j in range(nsteps):
-                fn(j)
-            ev[1].record()
-            torch.cuda.synchronize()
-            return ev[0].elapsed_time(ev[1]) / nsteps * 1e3
-
         fixed = {}
         for kb in (1024, 2048):
             ws_b = torch.zeros(bpc.decode_workspace_bytes(B, Hq, Hkv, N, L, kb), dtype=torch.uint8, device=dev)
@@ -326,7 +460,7 @@ def main():
                 bpc.decode_attention(it["q"], it["K"], it["V"], it["codes"], it["P"], kb, sm, out=outs[j % len(insts)],
                                      workspace=ws_b)
 
-            fixed[f"k{kb}_us_per_step"] = round(timed(fixed_step, max(10, min(args.steps, 100))), 2)
+            fixed[f"k{kb}_us_per_step"] = round(time_steps(fixed_step, prof_steps, args.warmup)[0], 2)
             del ws_b
         fixed["what"] = "the decode step with a fixed budget of 1024 or 2048 keys per (b, h)"
         log(f"fixed budgets: {fixed}")
@@ -339,7 +473,7 @@ def main():
             bpc.decode_attention_per_head(it["q"], it["K"], it["V"], it["codes"], it["P"], k, sm,
                                           out=outs[j % len(insts)], workspace=ws_ph)
 
-        ph_us = timed(per_head_step, max(10, min(args.steps, 100)))
+        ph_us = time_steps(per_head_step, prof_steps, args.warmup)[0]
         ph_bytes = B * Hq * N * W * 4 + B * Hq * k * 2 * D * 2 + B * Hq * L * D * 4 + B * Hq * D * (2 + 4)
         per_head = {"us_per_step": round(ph_us, 2), "GBps": round(ph_bytes / (ph_us * 1e-6) / 1e9, 1),
                     "what": f"one selection of {k} keys per query head ({Hq // Hkv} scans of each KV head's codes and "
@@ -348,21 +482,13 @@ def main():
         log(f"per query head: {per_head}")
 
         # ---------------------------------------------------------------- dense decode attention (context)
-        # full attention over all 131072 keys of every (b, h): what the sparse
-        # step replaces (the paper quotes its speed-ups against dense attention)
         ws_dense = torch.empty(int(bpc._lib.bpc_dense_workspace_bytes(B, Hq, Hkv, N, D)), dtype=torch.uint8, device=dev)
-        for j in range(3):
+
+        def dense_step(j):
             it = insts[j % len(insts)]
             bpc.dense_attention(it["q"], it["K"], it["V"], sm, out=outs[j % len(insts)], workspace=ws_dense)
-        dense_steps = 10
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for j in range(dense_steps):
-            it = insts[j % len(insts)]
-            bpc.dense_attention(it["q"], it["K"], it["V"], sm, out=outs[j % len(insts)], workspace=ws_dense)
-        e1.record()
-        torch.cuda.synchronize()
-        dense_us = e0.elapsed_time(e1) / dense_steps * 1e3
+
+        dense_us = time_steps(dense_step, 10, 3)[0]
         dense_bytes = B * Hkv * N * 2 * D * 2 + B * Hq * D * (2 + 4)
         dense = {"us_per_step": round(dense_us, 1), "GBps": round(dense_bytes / (dense_us * 1e-6) / 1e9, 1),
                  "sparse_speedup": round(dense_us / (ms_per_step * 1e3), 2),
@@ -371,10 +497,6 @@ def main():
         log(f"dense: {dense}")
 
         # ---------------------------------------------------------------- offline projection calibration (context)
-        # one P per KV head built offline (Algorithm 1 over held-out keys), then
-        # the batch's prefill is Algorithm 2 against it and decode reads it with
-        # a zero batch stride
-        opc = {}
         if not args.no_prefill:
             Kcal = make_calibration_keys(cfg, layer=0, n_seq=1, device=dev)
             ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
@@ -386,18 +508,11 @@ def main():
             torch.cuda.synchronize()
             del Kcal
             it = insts[0]
-            for j in range(5):
-                bpc.decode_attention(it["q"], it["K"], it["V"], codes_opc, Pcal, k, sm, out=outs[0], workspace=ws)
-            nrep = 50
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record()
-            for j in range(nrep):
-                bpc.decode_attention(it["q"], it["K"], it["V"], codes_opc, Pcal, k, sm, out=outs[0], workspace=ws)
-            e1.record()
-            torch.cuda.synchronize()
+            opc_us = time_steps(lambda j: bpc.decode_attention(it["q"], it["K"], it["V"], codes_opc, Pcal, k, sm,
+                                                               out=outs[0], workspace=ws), 50, 5)[0]
             opc = {"calibration_build_ms": round(ev[0].elapsed_time(ev[1]), 3),
                    "prefill_hash_ms": round(ev[1].elapsed_time(ev[2]), 3),
-                   "decode_us_per_step_same_instance": round(e0.elapsed_time(e1) / nrep * 1e3, 2),
+                   "decode_us_per_step_same_instance": round(opc_us, 2),
                    "what": "P per KV head from Algorithm 1 over 131072 held-out keys; prefill = Algorithm 2 of the "
                            "whole batch against it; decode with the shared P, one instance repeated (its data "
                            "partly stays in the 256 MB last-level cache)"}
@@ -410,13 +525,18 @@ def main():
     gather_bytes = BH * k * 2 * D * 2
     p_bytes = BH * L * D * 4
     qo_bytes = B * Hq * D * (2 + 4)
-    step_bytes = code_bytes + gather_bytes + p_bytes + qo_bytes
-    # the scoring kernel also packs the query (P and q of every (b, h))
-    per_kernel_bytes = {"score": code_bytes + p_bytes + B * Hq * D * 2, "attend": gather_bytes + B * Hq * D * 2}
-    # dominant kernel: the stage with the largest time among the HBM streamers
-    dom = max(("score", "attend"), key=lambda n: stages[n])
-    dom_us = stages[dom]
-    achieved = per_kernel_bytes[dom] / (dom_us * 1e-6) / 1e9
+    sbytes = code_bytes + gather_bytes + p_bytes + qo_bytes
+    if fused:
+        # one launch per step moves every algorithmic byte of the step: its
+        # average duration is the timed regions' step time (back-to-back
+        # launches; the event-bracketed stage timing adds each launch's
+        # end-of-kernel flush and is kept only as a breakdown)
+        dom, dom_us, dom_bytes = "fused_decode", float(np.median(runs)), sbytes
+    else:
+        per_kernel_bytes = {"score": code_bytes + p_bytes + B * Hq * D * 2, "attend": gather_bytes + B * Hq * D * 2}
+        dom = max(("score", "attend"), key=lambda n: stages[n])
+        dom_us, dom_bytes = stages[dom], per_kernel_bytes[dom]
+    achieved = dom_bytes / (dom_us * 1e-6) / 1e9
     traffic = None
     if os.path.exists(PMC_FILE):
         pmc = json.load(open(PMC_FILE))
@@ -424,13 +544,26 @@ def main():
             traffic = pmc["kernels"][dom]["hbm_bytes_per_launch"]
     roofline = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
-                "algorithmic_bytes_per_launch": per_kernel_bytes[dom], "avg_launch_us": dom_us}
-    step_gbs = step_bytes / (ms_per_step * 1e-3) / 1e9
+                "algorithmic_bytes_per_launch": dom_bytes, "avg_launch_us": round(dom_us, 2)}
+    step_gbs = sbytes / (ms_per_step * 1e-3) / 1e9
+
+    # ---------------------------------------------------------------- the other workloads
+    del insts, ws, outs
+    torch.cuda.empty_cache()
+    configs = {}
+    if not args.no_configs:
+        for name, n_inst, steps in (("tiny_mha_4k", 4, 200), ("llama8b_32k", 4, 200), ("stack32_b8_64k", 1, 10),
+                                    ("million_1m", 3, 60)):
+            configs[name] = measure_config(bpc, config_by_name(name), dev, n_inst, steps, 5, name)
+    ceiling = copy_ceiling(dev)
+    log(f"copy ceiling: {ceiling}")
 
     # ---------------------------------------------------------------- CPU oracle baseline
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(cfg, insts[0], args.cpu_sample_heads)
+        d0 = make_layer(cfg, layer=0, device=dev)
+        cpu = cpu_baseline(cfg, d0, args.cpu_sample_heads, host)
+        del d0
 
     line = {
         "metric": METRIC,
@@ -443,28 +576,37 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "u32+f32",
+        "dtype": "bf16 K/V/q, u32 codes, f32 accumulation",
         "data": "synthetic",
         "config": {"workload": cfg.name, "B": B, "Hq": Hq, "Hkv": Hkv, "head_dim": D, "N": N, "code_bits": L,
-                   "k": k, "budget": "2%", "instances": args.instances},
+                   "k": k, "budget": "2%", "instances": args.instances,
+                   "decode_path": "fused single launch" if fused else "three launches"},
+        "runs_us_per_step": [round(x, 2) for x in runs],
+        "median_us_per_step": round(float(np.median(runs)), 2),
+        "mean_us_per_step": round(float(np.mean(runs)), 2),
         "hbm_frac_step": round(step_gbs / HBM_PEAK_GBS, 4),
-        "step_algorithmic_bytes": step_bytes,
+        "step_algorithmic_bytes": sbytes,
         "step_GBps": round(step_gbs, 1),
+        "token_positions_per_s": B * N / (ms_per_step * 1e-3),
         "stages_us": stages,
+        "three_launch_path": {"us_per_step": round(three_us, 2), "stages_us": three},
         "roofline": roofline,
+        "copy_ceiling": ceiling,
         "prefill": prefill,
+        "configs": configs,
         "eas": eas,
         "fixed_budget": fixed,
         "per_query_head": per_head,
         "dense": dense,
         "opc": opc,
         "cpu_baseline": cpu,
+        "host": host,
         "wall_s_timed": round(wall, 4),
     }
     print(json.dumps(line), flush=True)
 
 
-def cpu_baseline(cfg, inst, heads: int):
+def cpu_baseline(cfg, inst, heads: int, host):
     """The oracle's decode step, timed on host cores for `heads` (b, h) pairs
     of the same workload.  Codes are drawn uniformly by the input generator
     (the oracle's running time does not depend on their values); P comes from
@@ -496,7 +638,8 @@ def cpu_baseline(cfg, inst, heads: int):
     keys = len(pairs) * cfg.N
     return {"value": keys / total, "unit": "keys/s", "cores": 1, "kind": "oracle",
             "sample": f"decode step of {len(pairs)} of the {cfg.B * cfg.Hkv} (sequence, KV head) pairs "
-                      f"({keys} keys) of {cfg.name}, numpy fp64 oracle on one thread, {total:.1f} s"}
+                      f"({keys} keys) of {cfg.name}, numpy fp64 oracle on one thread, {total:.1f} s",
+            "cpu_model": host["cpu_model"], "usable_cores": host["usable_cores"]}
 
 
 if __name__ == "__main__":

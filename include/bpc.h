@@ -88,6 +88,15 @@ int bpc_version(void);
 int bpc_set_decode_path(int path);
 
 /*
+ * bpc_decode_path_taken -- which path a decode step of this shape would take
+ * on the current device under the current bpc_set_decode_path setting:
+ * 0 = one fused launch, 1 = three launches.  Queries the device's occupancy
+ * (the first query per device and kernel instance); shapes the decode entry
+ * points reject return 1.
+ */
+int bpc_decode_path_taken(int B, int Hq, int Hkv, int N, int L);
+
+/*
  * bpc_build_hash -- binary principal components of each (sequence, KV
  * head)'s keys (Sec. 3.2, "Binary Principal Components Finding", Algorithm
  * "Constructing hash codes and corresponding hashing projection"; the

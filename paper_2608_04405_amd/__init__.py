@@ -35,6 +35,7 @@ __all__ = [
     "DECODE_STAGE_NAMES",
     "version",
     "set_decode_path",
+    "decode_path_taken",
     "DECODE_ZEROED_BYTES",
 ]
 
@@ -86,6 +87,8 @@ _lib.bpc_select_hard.restype = _i
 _lib.bpc_select_hard.argtypes = [_p, _i64, _i64, _i, _i, _i, _i, _p, _p]
 _lib.bpc_set_decode_path.restype = _i
 _lib.bpc_set_decode_path.argtypes = [_i]
+_lib.bpc_decode_path_taken.restype = _i
+_lib.bpc_decode_path_taken.argtypes = [_i, _i, _i, _i, _i]
 _lib.bpc_decode_noalloc_max_bytes.restype = _sz
 _lib.bpc_decode_noalloc_max_bytes.argtypes = []
 _lib.bpc_decode_attention_noalloc.restype = _i
@@ -121,6 +124,12 @@ def set_decode_path(path: int) -> None:
     """0: a decode step runs as one fused launch whenever its workgroups fit
     on the GPU at once (the default); 1: always the three launches."""
     _check(_lib.bpc_set_decode_path(int(path)), "bpc_set_decode_path")
+
+
+def decode_path_taken(B: int, Hq: int, Hkv: int, N: int, L: int) -> int:
+    """0 if a decode step of this shape runs as one fused launch on the
+    current device, 1 if as three launches (needs a GPU)."""
+    return int(_lib.bpc_decode_path_taken(B, Hq, Hkv, N, L))
 
 
 def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:

@@ -156,6 +156,11 @@ int bpc_set_decode_path(int path) {
   return BPC_OK;
 }
 
+int bpc_decode_path_taken(int B, int Hq, int Hkv, int N, int L) {
+  if (B < 1 || Hq < 1 || Hkv < 1 || N < 1 || (L != 32 && L != 64 && L != 128)) return 1;
+  return decode_fused_ok(B, Hq, Hkv, N, L) ? 0 : 1;
+}
+
 size_t bpc_build_workspace_bytes(int B, int Hkv, int N, int D, int L) {
   if (B < 1 || Hkv < 1 || N < 1 || D != kHeadDim) return 0;
   return build_layout(B, Hkv, N, L).total;
