@@ -221,7 +221,7 @@ int bpc_append_kv(const uint16_t* k_new, int64_t sKn_b, int64_t sKn_h, int64_t s
  * score_out  [B, Hkv, N] int32 scores c_n (or NULL)
  * qcode_out  [B, Hkv, 8, W] uint32 packed query planes (or NULL)
  * workspace  at least bpc_decode_workspace_bytes(...) bytes, 256-byte
- *            aligned.  Its first 256 KiB (BPC_DECODE_ZEROED_BYTES) must be
+ *            aligned.  Its first 1088 KiB (BPC_DECODE_ZEROED_BYTES) must be
  *            zero before the first call on it (allocate it zeroed); every
  *            call leaves them zero.  The rest may hold anything.  Two calls
  *            that use the same workspace must be ordered on one stream.
@@ -236,7 +236,7 @@ int bpc_append_kv(const uint16_t* k_new, int64_t sKn_b, int64_t sKn_h, int64_t s
  * for a ragged last slice or codes whose strides are not multiples of 4
  * words.  bpc_set_decode_path selects the three launches for comparisons.
  */
-#define BPC_DECODE_ZEROED_BYTES (256u * 1024u)
+#define BPC_DECODE_ZEROED_BYTES (1088u * 1024u)
 size_t bpc_decode_workspace_bytes(int B, int Hq, int Hkv, int N, int D, int L, int k);
 int bpc_decode_attention(const uint16_t* q,
                          const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t sK_n,

@@ -100,7 +100,7 @@ DECODE_STAGES = 3
 DECODE_STAGE_NAMES = ("score", "attend", "merge")
 # a decode workspace's leading bytes that must be zero before its first use
 # (the fused path's arrival counters; every call leaves them zero)
-DECODE_ZEROED_BYTES = 256 * 1024
+DECODE_ZEROED_BYTES = 1088 * 1024
 
 
 class BPCError(RuntimeError):

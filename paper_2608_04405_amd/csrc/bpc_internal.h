@@ -54,10 +54,15 @@ constexpr int kWinSlices = 64;             // slices per (b, h) the one-round th
 constexpr int kFusedSyncWords = 16;
 constexpr int kFusedPubWords = kWinRec + 4 + kCoarseStride + 128;
 // The counters sit in a fixed region at the start of every decode workspace
-// (either path), for up to kFusedMaxBH (b, h) pairs; the three-launch path
-// never writes it, so it stays zero once zeroed.
-constexpr int kFusedMaxBH = 4096;
-constexpr size_t kSyncRegionBytes = (size_t)kFusedMaxBH * kFusedSyncWords * sizeof(uint32_t);
+// (either path), for up to kFusedMaxBH (b, h) pairs, followed by the
+// projected query rows the slices of a (b, h) share (kFusedMaxL fp64 rows per
+// (b, h), zero while no step runs); the three-launch path never writes the
+// region, so it stays zero once zeroed.  (More (b, h) pairs than the fused
+// grid's workgroups never take the fused path anyway.)
+constexpr int kFusedMaxBH = 1024;
+constexpr int kFusedMaxL = 128;
+constexpr size_t kSyncCounterBytes = (size_t)kFusedMaxBH * kFusedSyncWords * sizeof(uint32_t);
+constexpr size_t kSyncRegionBytes = kSyncCounterBytes + (size_t)kFusedMaxBH * kFusedMaxL * sizeof(uint64_t);
 
 // ---- build tiling ----------------------------------------------------------
 constexpr int kBuildGroups = 2;                  // groups of 64 keys per build workgroup

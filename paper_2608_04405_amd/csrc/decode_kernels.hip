@@ -249,6 +249,48 @@ __device__ __forceinline__ void qpack_block(QpackShared<L, GMAX>& sh, QpackOut<L
   __syncthreads();
 }
 
+// The group sum of one row of P for the quad lane c that holds coordinates
+// [32 c, 32 c + 32) of the row in pv (fp32, in coordinate order), with the
+// group's queries in qs: the same fixed-order arithmetic as qpack_block (per
+// head a sequential fp64 chain over the lane's 32 coordinates, the quad's
+// four chains added as (c0 + c1) + (c2 + c3), the heads in ascending order).
+// All four lanes of the quad must be active; each returns the row's value.
+template <int G>
+__device__ __forceinline__ double quad_row_sum(const float4 (&pv)[8], int c, const uint4 (*qs)[kHeadDim / 8]) {
+  double xb = 0.0;
+#pragma unroll
+  for (int g0 = 0; g0 < G; g0 += 4) {
+    double acc[4] = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const float pf[8] = {pv[2 * j].x, pv[2 * j].y, pv[2 * j].z, pv[2 * j].w,
+                           pv[2 * j + 1].x, pv[2 * j + 1].y, pv[2 * j + 1].z, pv[2 * j + 1].w};
+      uint32_t w4[4][4];
+#pragma unroll
+      for (int hh = 0; hh < 4; ++hh) {
+        const uint4 qq = qs[g0 + hh < G ? g0 + hh : g0][4 * c + j];
+        w4[hh][0] = qq.x, w4[hh][1] = qq.y, w4[hh][2] = qq.z, w4[hh][3] = qq.w;
+      }
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const double d0 = (double)pf[2 * e], d1 = (double)pf[2 * e + 1];
+#pragma unroll
+        for (int hh = 0; hh < 4; ++hh) {
+          acc[hh] = __builtin_fma(d0, (double)bf16_to_f32(w4[hh][e] & 0xFFFFu), acc[hh]);
+          acc[hh] = __builtin_fma(d1, (double)bf16_to_f32(w4[hh][e] >> 16), acc[hh]);
+        }
+      }
+    }
+#pragma unroll
+    for (int hh = 0; hh < 4; ++hh) {
+      const double s01 = dadd(acc[hh], dpp_f64<kDppQuadXor1>(acc[hh]));
+      const double a = dadd(s01, dpp_f64<kDppQuadXor2>(s01));
+      if (g0 + hh < G) xb = (g0 + hh == 0) ? a : dadd(xb, a);
+    }
+  }
+  return xb;
+}
+
 // ---------------------------------------------------------------------------
 // 1. score -- one 512-thread workgroup per slice.
 // The workgroup first packs its (b, h)'s query group (above).  Each thread
@@ -276,17 +318,18 @@ __device__ __forceinline__ u32x4_t load_code_group(const uint32_t* cb, int n, in
 }
 
 // weighted Hamming distance sum_j 2^j popc(M_j & (code ^ s)) of key u of a
-// 16-byte group
+// 16-byte group, by Horner's rule over the planes (most significant first:
+// d = 2 d + popcounts of plane j), so that every popcount accumulates into d
+// (one AND-XOR and one popcount per plane and word, one shift per plane)
 template <int W>
 __device__ __forceinline__ uint32_t code_distance(const u32x4_t cw, int u, const uint32_t (&M)[7][W],
                                                   const uint32_t (&sg)[W]) {
   uint32_t d = 0;
 #pragma unroll
-  for (int j = 0; j < 7; ++j) {
-    uint32_t pc = 0;
+  for (int j = 6; j >= 0; --j) {
+    d += d;
 #pragma unroll
-    for (int w = 0; w < W; ++w) pc += __popc(M[j][w] & (cw[u * W + w] ^ sg[w]));
-    d += pc << j;
+    for (int w = 0; w < W; ++w) d = (uint32_t)__popc(M[j][w] & (cw[u * W + w] ^ sg[w])) + d;
   }
   return d;
 }
@@ -594,11 +637,13 @@ __device__ __forceinline__ void score_body(ScoreShared<L>& sh, int bh, int s, co
   if (threadIdx.x == 0) *reinterpret_cast<uint4*>(meta + sl * 4) = make_uint4(kth, cmin, total, cand_max);
   if (score_out) {  // debug output
     int32_t* so = score_out + (size_t)bh * N + n0;
+    int kb = wid * KPW + lane * KPL;  // opaque: no per-key offsets are kept from the scoring loop
+    __asm__ volatile("" : "+v"(kb));
 #pragma unroll
     for (int it = 0; it < NLD; ++it)
 #pragma unroll
       for (int u = 0; u < KPL; ++u) {
-        const int n = key_of(it, u);
+        const int n = kb + it * KSTEP + u;
         if (n < cnt) so[n] = T - 2 * dist_of(it, u);
       }
   }
@@ -721,29 +766,57 @@ __device__ __forceinline__ void pin_regs(uint4& x) {
 // lands in lane (r, head) for rows 4 r .. 4 r + 3.  V: lane (r, c) loads
 // dims [8 c, 8 c + 8) of rows 4 r .. 4 r + 3, which are exactly the rows
 // whose logits the lanes (r, head < G) of its own group hold.
-template <int G>
-__device__ __forceinline__ void attend_pass(uint32_t rk, const uint32_t (&rv)[4], int nrows,
-                                            const uint4 (*qs)[kHeadDim / 8], float (*pl)[16], const char* Kh,
-                                            uint32_t kstride, const char* Vh, uint32_t vstride, float scale_log2,
-                                            float (&Mx)[G], float (&Ls)[G], float (&o)[G][8]) {
-  static_assert(G <= 16, "the query heads of a group fill at most the 16 columns of a tile");
-  const int lane = threadIdx.x & 63;
-  const int c16 = lane & 15, r4 = lane >> 4;
-  // the rows are read once: non-temporal loads keep them from displacing
-  // what the caches hold for the other workgroups (measured: 4.5 us of the
-  // decode step at batch 16 x 8 x 131072 against plain loads)
-  uint4 kv[4], vv[4];
+// The pieces of one pass: the K loads, the V loads, the logits (from K) and
+// the softmax update with the weighted V (from V).  attend_pass runs them in
+// order; a pipelined caller issues the next pass's loads between them.  The
+// rows are read once: non-temporal loads keep them from displacing what the
+// caches hold for the other workgroups (measured: 4.5 us of the decode step
+// at batch 16 x 8 x 131072 against plain loads).
+__device__ __forceinline__ void attend_load_k(uint32_t rk, const char* Kh, uint32_t kstride, uint4 (&kv)[4]) {
+  const int r4 = (threadIdx.x & 63) >> 4;
 #pragma unroll
   for (int kb = 0; kb < 4; ++kb) {
     const u32x4_t x =
         __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(Kh + (rk * kstride + 64u * kb + 16u * r4)));
     kv[kb] = make_uint4(x[0], x[1], x[2], x[3]);
   }
+}
+__device__ __forceinline__ void attend_load_v(const uint32_t (&rv)[4], const char* Vh, uint32_t vstride,
+                                              uint4 (&vv)[4]) {
+  const int c16 = threadIdx.x & 15;
 #pragma unroll
   for (int t = 0; t < 4; ++t) {
     const u32x4_t x = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(Vh + (rv[t] * vstride + 16u * c16)));
     vv[t] = make_uint4(x[0], x[1], x[2], x[3]);
   }
+}
+
+template <int G>
+__device__ __forceinline__ void attend_logits(const uint4 (&kv)[4], int nrows, const uint4 (*qs)[kHeadDim / 8],
+                                              float (*pl)[16], float scale_log2);
+template <int G>
+__device__ __forceinline__ void attend_pv(const uint4 (&vv)[4], float (*pl)[16], float (&Mx)[G], float (&Ls)[G],
+                                          float (&o)[G][8]);
+
+template <int G>
+__device__ __forceinline__ void attend_pass(uint32_t rk, const uint32_t (&rv)[4], int nrows,
+                                            const uint4 (*qs)[kHeadDim / 8], float (*pl)[16], const char* Kh,
+                                            uint32_t kstride, const char* Vh, uint32_t vstride, float scale_log2,
+                                            float (&Mx)[G], float (&Ls)[G], float (&o)[G][8]) {
+  uint4 kv[4], vv[4];
+  attend_load_k(rk, Kh, kstride, kv);
+  attend_load_v(rv, Vh, vstride, vv);
+  attend_logits<G>(kv, nrows, qs, pl, scale_log2);
+  attend_pv<G>(vv, pl, Mx, Ls, o);
+}
+
+// Logits of the pass's rows (from their K) into the wavefront's LDS area pl.
+template <int G>
+__device__ __forceinline__ void attend_logits(const uint4 (&kv)[4], int nrows, const uint4 (*qs)[kHeadDim / 8],
+                                              float (*pl)[16], float scale_log2) {
+  static_assert(G <= 16, "the query heads of a group fill at most the 16 columns of a tile");
+  const int lane = threadIdx.x & 63;
+  const int c16 = lane & 15, r4 = lane >> 4;
   // logits on the matrix cores
   int qi = c16;
   __asm__ volatile("" : "+v"(qi));  // the query is re-read from LDS each pass, not held in registers
@@ -762,6 +835,14 @@ __device__ __forceinline__ void attend_pass(uint32_t rk, const uint32_t (&rv)[4]
     w.w = 4 * r4 + 3 < nrows ? acc[3] * scale_log2 : -INFINITY;
     *reinterpret_cast<float4*>(&pl[c16][4 * r4]) = w;
   }
+}
+
+// The running softmax and weighted V of the pass whose logits are in pl.
+template <int G>
+__device__ __forceinline__ void attend_pv(const uint4 (&vv)[4], float (*pl)[16], float (&Mx)[G], float (&Ls)[G],
+                                          float (&o)[G][8]) {
+  const int lane = threadIdx.x & 63;
+  const int r4 = lane >> 4;
   // LDS operations of one wavefront complete in order: the reads below see
   // the writes above; this only keeps the compiler from moving them across
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -825,6 +906,12 @@ __device__ __forceinline__ uint32_t pub_load(const uint32_t* p) {
 }
 // every store this thread has issued is complete before anything after it
 __device__ __forceinline__ void stores_complete() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+__device__ __forceinline__ void pub_store64(uint64_t* p, uint64_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint64_t pub_load64(const uint64_t* p) {
+  return __hip_atomic_load(const_cast<uint64_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
 
 // The workgroup's partial for each query head g: each wavefront reduces its
 // weighted V over its four row groups; the wavefronts are combined under
@@ -1582,8 +1669,74 @@ __global__ __launch_bounds__(kFusedThreads) __attribute__((amdgpu_waves_per_eu(f
     return load_code_group<W>(cb, n, cnt, (reinterpret_cast<uintptr_t>(cb) & 15u) == 0);
   };
   u32x4_t cw[RD];
-  qpack_block<L, NT, G>(sh.u.qp, sh.qo, q + ((size_t)b * Hkv * G + (size_t)h * G) * kHeadDim, P + b * sP_b + h * sP_h,
-                        G, [&]() { cw[0] = load_group(0); });
+  const uint16_t* qg = q + ((size_t)b * Hkv * G + (size_t)h * G) * kHeadDim;
+  const float* Pbh = P + b * sP_b + h * sP_h;
+  // the (b, h)'s shared query rows (an expression, not a value kept live)
+  auto xq_of = [&]() {
+    return reinterpret_cast<uint64_t*>(sync + (size_t)kFusedMaxBH * kFusedSyncWords) + (size_t)bh * kFusedMaxL;
+  };
+  if (nslices == 1) {
+    qpack_block<L, NT, G>(sh.u.qp, sh.qo, qg, Pbh, G, [&]() { cw[0] = load_group(0); });
+  } else {
+    // The slices of (b, h) share the projection: slice s computes rows
+    // [s R, s R + R) of the group sum (R = ceil(L / nslices)) and publishes
+    // them (bit-complemented, so that a published row is never zero); every
+    // slice then collects all L rows and quantises them itself.  The rows go
+    // back to zero when the step's merge ends.
+    const int R = (L + nslices - 1) / nslices;
+    const int r0 = s * R, nr = max(0, min(R, L - r0));
+    const int i = threadIdx.x >> 2, c = threadIdx.x & 3;  // quad i: row r0 + i
+    if (threadIdx.x < G * (kHeadDim / 8))
+      sh.q[threadIdx.x / (kHeadDim / 8)][threadIdx.x % (kHeadDim / 8)] = reinterpret_cast<const uint4*>(qg)[threadIdx.x];
+    float4 pv[8];
+    if (i < nr) {
+      const float4* pr = reinterpret_cast<const float4*>(Pbh + (size_t)(r0 + i) * kHeadDim + 32 * c);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) pv[j] = pr[j];
+    }
+    cw[0] = load_group(0);
+    __syncthreads();  // the queries
+    BPC_STAMP(1, 6);
+    if (i < nr) {
+      const double x = quad_row_sum<G>(pv, c, sh.q);
+      if (c == 0) pub_store64(xq_of() + r0 + i, ~(uint64_t)__double_as_longlong(x));
+    }
+    if (wid == 0) {
+      // every row published (rows at or past L count as present)
+      uint64_t v0 = lane < L ? 0u : 1u, v1 = lane + 64 < L ? 0u : 1u;
+      unsigned it = 0;
+      for (;;) {
+        if (v0 == 0u) v0 = pub_load64(xq_of() + lane);
+        if (v1 == 0u) v1 = pub_load64(xq_of() + 64 + lane);
+        if (__all(v0 != 0u && v1 != 0u) || ++it >= kSpinLimit) break;
+        __builtin_amdgcn_s_sleep(2);
+      }
+      // a row still missing after the bounded wait counts as zero
+      const double x0 = (lane < L && v0 != 0u) ? __longlong_as_double((long long)~v0) : 0.0;
+      const double x1 = (lane + 64 < L && v1 != 0u) ? __longlong_as_double((long long)~v1) : 0.0;
+      double m = fmax(fabs(x0), fabs(x1));
+#pragma unroll
+      for (int off = 32; off >= 1; off >>= 1) {
+        const int lo = __shfl_xor(__double2loint(m), off), hi = __shfl_xor(__double2hiint(m), off);
+        m = fmax(m, __hiloint2double(hi, lo));
+      }
+      const int p0 = (m > 0.0) ? (int)round(dmul(x0, 127.0) / m) : 0;
+      const int p1 = (m > 0.0) ? (int)round(dmul(x1, 127.0) / m) : 0;
+      uint32_t* qw = reinterpret_cast<uint32_t*>(sh.qo.qc16);
+#pragma unroll
+      for (int plane = 0; plane < 8; ++plane) {
+        const bool on0 = plane == 0 ? (p0 >= 0) : (((uint32_t)abs(p0) >> (plane - 1)) & 1u) != 0u;
+        const bool on1 = plane == 0 ? (p1 >= 0) : (((uint32_t)abs(p1) >> (plane - 1)) & 1u) != 0u;
+        const unsigned long long m0 = __ballot(on0 && lane < L), m1 = __ballot(on1 && lane + 64 < L);
+        if (lane == 0) {
+          qw[plane * W] = (uint32_t)m0;
+          if (W > 1) qw[plane * W + 1] = (uint32_t)(m0 >> 32);
+          if (W > 2) qw[plane * W + 2] = (uint32_t)m1, qw[plane * W + 3] = (uint32_t)(m1 >> 32);
+        }
+      }
+    }
+    __syncthreads();
+  }
   BPC_STAMP(1, 1);
   const uint32_t* qcw = reinterpret_cast<const uint32_t*>(sh.qo.qc16);
   uint32_t sg[W], M[7][W];
@@ -1604,18 +1757,36 @@ __global__ __launch_bounds__(kFusedThreads) __attribute__((amdgpu_waves_per_eu(f
   __syncthreads();
   // distances (< 2^14) two per register: key i = it * KPL + u is half i & 1 of dpk[i >> 1]
   uint32_t dpk[PER / 2];
+  if (full) {  // every key of the slice present, every load one 16-byte load: no per-key tests
 #pragma unroll
-  for (int it = 0; it < NLD; ++it) {
-    const u32x4_t c = cw[it % RD];
-    if (it + RD < NLD) cw[it % RD] = load_group(it + RD);
+    for (int it = 0; it < NLD; ++it) {
+      const u32x4_t c = cw[it % RD];
+      if (it + RD < NLD)
+        cw[it % RD] = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(
+            reinterpret_cast<const char*>(cb) + (uint32_t)key_of(it + RD, 0) * (4u * W)));
 #pragma unroll
-    for (int u = 0; u < KPL; ++u) {
-      const bool valid = key_of(it, u) < cnt;
-      const uint32_t d = valid ? code_distance<W>(c, u, M, sg) : 0xFFFFu;
-      const int i = it * KPL + u;
-      dpk[i >> 1] = (i & 1) ? (dpk[i >> 1] | (d << 16)) : d;
-      if (i & 1) __asm__ volatile("" : "+v"(dpk[i >> 1]));
-      if (valid) atomicAdd(&sh.u.hist[d], 1u);
+      for (int u = 0; u < KPL; ++u) {
+        const uint32_t d = code_distance<W>(c, u, M, sg);
+        const int i = it * KPL + u;
+        dpk[i >> 1] = (i & 1) ? (dpk[i >> 1] | (d << 16)) : d;
+        if (i & 1) __asm__ volatile("" : "+v"(dpk[i >> 1]));
+        atomicAdd(&sh.u.hist[d], 1u);
+      }
+    }
+  } else {
+#pragma unroll
+    for (int it = 0; it < NLD; ++it) {
+      const u32x4_t c = cw[it % RD];
+      if (it + RD < NLD) cw[it % RD] = load_group(it + RD);
+#pragma unroll
+      for (int u = 0; u < KPL; ++u) {
+        const bool valid = key_of(it, u) < cnt;
+        const uint32_t d = valid ? code_distance<W>(c, u, M, sg) : 0xFFFFu;
+        const int i = it * KPL + u;
+        dpk[i >> 1] = (i & 1) ? (dpk[i >> 1] | (d << 16)) : d;
+        if (i & 1) __asm__ volatile("" : "+v"(dpk[i >> 1]));
+        if (valid) atomicAdd(&sh.u.hist[d], 1u);
+      }
     }
   }
   __syncthreads();
@@ -1632,11 +1803,13 @@ __global__ __launch_bounds__(kFusedThreads) __attribute__((amdgpu_waves_per_eu(f
   };
   if (score_out) {  // debug output
     int32_t* so = score_out + (size_t)bh * N + n0;
+    int kb = wid * KPW + lane * KPL;  // opaque: no per-key offsets are kept from the scoring loop
+    __asm__ volatile("" : "+v"(kb));
 #pragma unroll
     for (int it = 0; it < NLD; ++it)
 #pragma unroll
       for (int u = 0; u < KPL; ++u) {
-        const int n = key_of(it, u);
+        const int n = kb + it * KSTEP + u;
         if (n < cnt) so[n] = T - 2 * dist_of(it, u);
       }
   }
@@ -2242,8 +2415,10 @@ __global__ __launch_bounds__(kFusedThreads) __attribute__((amdgpu_waves_per_eu(f
     }
     out[((size_t)b * Hkv * G + (size_t)h * G + g) * kHeadDim + d] = acc / lsum;
   }
-  // every slice of (b, h) has passed both waits: the counters go back to zero
+  // every slice of (b, h) has passed every wait: the counters and the shared
+  // query rows go back to zero
   if (threadIdx.x < 3) __hip_atomic_store(bh_sync + threadIdx.x, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (nslices > 1 && threadIdx.x < L) pub_store64(xq_of() + threadIdx.x, 0u);
   BPC_STAMP(1, 10);
 }
 

@@ -315,7 +315,7 @@ def test_decode_threshold_below_the_windows():
 
 
 def test_decode_garbage_workspace():
-    """Only the workspace's counter region (its first 256 KiB) needs zeroing
+    """Only the workspace's counter region (its first DECODE_ZEROED_BYTES) needs zeroing
     once: a first call on a workspace holding random bytes elsewhere, and
     later calls on the same workspace, all match the oracle, on the fused
     path and on the three-launch path."""
