@@ -793,27 +793,35 @@ __device__ __forceinline__ void attend_load_v(const uint32_t (&rv)[4], const cha
 
 template <int G>
 __device__ __forceinline__ void attend_logits(const uint4 (&kv)[4], int nrows, const uint4 (*qs)[kHeadDim / 8],
-                                              float (*pl)[16], float scale_log2);
+                                              float (*pl)[16], float scale_log2, float& mx, float& ls, float& f);
 template <int G>
-__device__ __forceinline__ void attend_pv(const uint4 (&vv)[4], float (*pl)[16], float (&Mx)[G], float (&Ls)[G],
-                                          float (&o)[G][8]);
+__device__ __forceinline__ void attend_pv(const uint4 (&vv)[4], float (*pl)[16], float f, float (&o)[G][8]);
 
+// mx, ls: the running (max, sum) of query head lane % 16 (lanes below G)
 template <int G>
 __device__ __forceinline__ void attend_pass(uint32_t rk, const uint32_t (&rv)[4], int nrows,
                                             const uint4 (*qs)[kHeadDim / 8], float (*pl)[16], const char* Kh,
                                             uint32_t kstride, const char* Vh, uint32_t vstride, float scale_log2,
-                                            float (&Mx)[G], float (&Ls)[G], float (&o)[G][8]) {
+                                            float& mx, float& ls, float (&o)[G][8]) {
   uint4 kv[4], vv[4];
   attend_load_k(rk, Kh, kstride, kv);
   attend_load_v(rv, Vh, vstride, vv);
-  attend_logits<G>(kv, nrows, qs, pl, scale_log2);
-  attend_pv<G>(vv, pl, Mx, Ls, o);
+  float f;
+  attend_logits<G>(kv, nrows, qs, pl, scale_log2, mx, ls, f);
+  attend_pv<G>(vv, pl, f, o);
 }
 
-// Logits of the pass's rows (from their K) into the wavefront's LDS area pl.
+// Logits of the pass's rows (from their K) and the running softmax update,
+// computed in the lanes that hold them: lane (r, g) = (lane / 16, lane % 16),
+// g < G, has the logits of rows 4 r .. 4 r + 3 for query head g and keeps head
+// g's running maximum mx and sum ls (the same in its four row groups).  The
+// pass's probabilities go to the wavefront's LDS area pl; the rescale factor
+// of earlier passes comes back per head.  The arithmetic is that of a
+// wavefront-uniform update: the maximum over the four row groups, then
+// exp2(logit - max), the group sums added as ((r0 + r1) + (r2 + r3)).
 template <int G>
 __device__ __forceinline__ void attend_logits(const uint4 (&kv)[4], int nrows, const uint4 (*qs)[kHeadDim / 8],
-                                              float (*pl)[16], float scale_log2) {
+                                              float (*pl)[16], float scale_log2, float& mx, float& ls, float& f) {
   static_assert(G <= 16, "the query heads of a group fill at most the 16 columns of a tile");
   const int lane = threadIdx.x & 63;
   const int c16 = lane & 15, r4 = lane >> 4;
@@ -827,22 +835,51 @@ __device__ __forceinline__ void attend_logits(const uint4 (&kv)[4], int nrows, c
     acc = mfma16(kv[kb].x, kv[kb].y, qv.x, qv.y, acc);
     acc = mfma16(kv[kb].z, kv[kb].w, qv.z, qv.w, acc);
   }
-  if (c16 < G) {
-    float4 w;
-    w.x = 4 * r4 + 0 < nrows ? acc[0] * scale_log2 : -INFINITY;
-    w.y = 4 * r4 + 1 < nrows ? acc[1] * scale_log2 : -INFINITY;
-    w.z = 4 * r4 + 2 < nrows ? acc[2] * scale_log2 : -INFINITY;
-    w.w = 4 * r4 + 3 < nrows ? acc[3] * scale_log2 : -INFINITY;
-    *reinterpret_cast<float4*>(&pl[c16][4 * r4]) = w;
+  float x[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) x[j] = 4 * r4 + j < nrows ? acc[j] * scale_log2 : -INFINITY;
+  // the pass's maximum over the 16 rows: the lane's four, then across the row groups
+  float m = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
+  {
+    const auto p16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(m), __float_as_uint(m), false, false);
+    m = fmaxf(__uint_as_float(p16[0]), __uint_as_float(p16[1]));
+    const auto p32 = __builtin_amdgcn_permlane32_swap(__float_as_uint(m), __float_as_uint(m), false, false);
+    m = fmaxf(__uint_as_float(p32[0]), __uint_as_float(p32[1]));
   }
+  const float mnew = fmaxf(mx, m);
+  // rescale what earlier passes accumulated (mx = -inf before the first: factor 0)
+  f = (mx == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mx - mnew);
+  float ps = 0.f;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    x[j] = __builtin_amdgcn_exp2f(x[j] - mnew);  // a masked row: exp2(-inf) = 0
+    ps += x[j];
+  }
+  {
+    const auto p16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(ps), __float_as_uint(ps), false, false);
+    const float y = __uint_as_float(p16[0]) + __uint_as_float(p16[1]);
+    const auto p32 = __builtin_amdgcn_permlane32_swap(__float_as_uint(y), __float_as_uint(y), false, false);
+    ps = __uint_as_float(p32[0]) + __uint_as_float(p32[1]);
+  }
+  ls = ls * f + ps;
+  mx = mnew;
+  if (c16 < G) *reinterpret_cast<float4*>(&pl[c16][4 * r4]) = make_float4(x[0], x[1], x[2], x[3]);
 }
 
-// The running softmax and weighted V of the pass whose logits are in pl.
+// The weighted V of the pass whose probabilities are in pl, after scaling
+// what earlier passes accumulated by each head's factor f (lane g holds
+// head g's).
 template <int G>
-__device__ __forceinline__ void attend_pv(const uint4 (&vv)[4], float (*pl)[16], float (&Mx)[G], float (&Ls)[G],
-                                          float (&o)[G][8]) {
+__device__ __forceinline__ void attend_pv(const uint4 (&vv)[4], float (*pl)[16], float f, float (&o)[G][8]) {
   const int lane = threadIdx.x & 63;
   const int r4 = lane >> 4;
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    const float fg = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(f), g));
+    if (fg != 1.f)  // a product with 1 changes nothing
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[g][e] *= fg;
+  }
   // LDS operations of one wavefront complete in order: the reads below see
   // the writes above; this only keeps the compiler from moving them across
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -857,32 +894,6 @@ __device__ __forceinline__ void attend_pv(const uint4 (&vv)[4], float (*pl)[16],
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();  // the next pass rewrites pl only after these reads
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-  // running maximum and sum, uniform over the wavefront: the lanes of a row
-  // group hold the same four rows, so lanes 0, 16, 32 and 48 carry the four
-  // groups' partial results
-#pragma unroll
-  for (int g = 0; g < G; ++g) {
-    float m = fmaxf(fmaxf(lg[g][0], lg[g][1]), fmaxf(lg[g][2], lg[g][3]));
-    const int mb = __float_as_int(m);
-    m = fmaxf(fmaxf(__int_as_float(__builtin_amdgcn_readlane(mb, 0)), __int_as_float(__builtin_amdgcn_readlane(mb, 16))),
-              fmaxf(__int_as_float(__builtin_amdgcn_readlane(mb, 32)), __int_as_float(__builtin_amdgcn_readlane(mb, 48))));
-    const float mnew = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(fmaxf(Mx[g], m))));
-    // rescale what earlier passes accumulated (Mx = -inf before the first: factor 0)
-    const float f = (Mx[g] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(Mx[g] - mnew);
-    float ps = 0.f;
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      lg[g][t] = __builtin_amdgcn_exp2f(lg[g][t] - mnew);  // a masked row: exp2(-inf) = 0
-      ps += lg[g][t];
-    }
-    const int pb = __float_as_int(ps);
-    ps = (__int_as_float(__builtin_amdgcn_readlane(pb, 0)) + __int_as_float(__builtin_amdgcn_readlane(pb, 16))) +
-         (__int_as_float(__builtin_amdgcn_readlane(pb, 32)) + __int_as_float(__builtin_amdgcn_readlane(pb, 48)));
-    Ls[g] = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(Ls[g] * f + ps)));
-    Mx[g] = mnew;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) o[g][e] *= f;
-  }
   // weighted V of the lane's rows
 #pragma unroll
   for (int t = 0; t < 4; ++t) {
@@ -892,6 +903,17 @@ __device__ __forceinline__ void attend_pv(const uint4 (&vv)[4], float (*pl)[16],
     for (int g = 0; g < G; ++g)
 #pragma unroll
       for (int e = 0; e < 8; ++e) o[g][e] = fmaf(lg[g][t], vf[e], o[g][e]);
+  }
+}
+
+// The running (max, sum) of each head as wavefront-uniform values, from the
+// lanes that hold them.
+template <int G>
+__device__ __forceinline__ void lane_stats(float mx, float ls, float (&Mx)[G], float (&Ls)[G]) {
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    Mx[g] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(mx), g));
+    Ls[g] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(ls), g));
   }
 }
 
@@ -1364,10 +1386,10 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(G 
   const char* Kh = reinterpret_cast<const char*>(K + b * sK_b + h * sK_h);
   const char* Vh = reinterpret_cast<const char*>(V + b * sV_b + h * sV_h);
   const uint32_t kstride = (uint32_t)sK_n * 2u, vstride = (uint32_t)sV_n * 2u;
-  float Mx[G], Ls[G], o[G][8];
+  float mx = -INFINITY, ls = 0.f;  // running (max, sum) of query head lane % 16 (lanes below G)
+  float o[G][8];
 #pragma unroll
   for (int g = 0; g < G; ++g) {
-    Mx[g] = -INFINITY, Ls[g] = 0.f;
 #pragma unroll
     for (int e = 0; e < 8; ++e) o[g][e] = 0.f;
   }
@@ -1389,14 +1411,14 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(G 
       const int nr = min(kAttnRows, kept - r0);
       uint32_t rk, rv[4];
       pass_rows(sh.u.rows, r0, nr, rk, rv);
-      attend_pass<G>(rk, rv, nr, sh.q, sh.pl[wid], Kh, kstride, Vh, vstride, scale_log2, Mx, Ls, o);
+      attend_pass<G>(rk, rv, nr, sh.q, sh.pl[wid], Kh, kstride, Vh, vstride, scale_log2, mx, ls, o);
     }
   } else {
     for (int r0 = wid * kAttnRows; r0 < kept; r0 += kAttnWaves * kAttnRows) {
       const int nr = min(kAttnRows, kept - r0);
       uint32_t rk, rv[4];
       pass_rows(grows, r0, nr, rk, rv);
-      attend_pass<G>(rk, rv, nr, sh.q, sh.pl[wid], Kh, kstride, Vh, vstride, scale_log2, Mx, Ls, o);
+      attend_pass<G>(rk, rv, nr, sh.q, sh.pl[wid], Kh, kstride, Vh, vstride, scale_log2, mx, ls, o);
     }
   }
   BPC_STAMP(2, 5);
@@ -1405,6 +1427,8 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(G 
   BPC_NOTE(2, 14, planned);
   __syncthreads();  // the row list is read to the end before its area holds o
 
+  float Mx[G], Ls[G];
+  lane_stats<G>(mx, ls, Mx, Ls);
   write_partial<G>(sh.u.o, sh.st, Mx, Ls, o, part + sl * G * (kHeadDim + 2));
   BPC_STAMP(2, 6);
 }
@@ -1442,10 +1466,10 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(G 
   const char* Kh = reinterpret_cast<const char*>(K + b * sK_b + h * sK_h);
   const char* Vh = reinterpret_cast<const char*>(V + b * sV_b + h * sV_h);
   const uint32_t kstride = (uint32_t)sK_n * 2u, vstride = (uint32_t)sV_n * 2u;
-  float Mx[G], Ls[G], o[G][8];
+  float mx = -INFINITY, ls = 0.f;  // running (max, sum) of query head lane % 16 (lanes below G)
+  float o[G][8];
 #pragma unroll
   for (int g = 0; g < G; ++g) {
-    Mx[g] = -INFINITY, Ls[g] = 0.f;
 #pragma unroll
     for (int e = 0; e < 8; ++e) o[g][e] = 0.f;
   }
@@ -1456,8 +1480,10 @@ __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(G 
     uint32_t rv[4];
 #pragma unroll
     for (int t = 0; t < 4; ++t) rv[t] = 4 * r4 + t < nr ? (uint32_t)(n0 + r0 + 4 * r4 + t) : 0u;
-    attend_pass<G>(rk, rv, nr, sh.q, sh.pl[wid], Kh, kstride, Vh, vstride, scale_log2, Mx, Ls, o);
+    attend_pass<G>(rk, rv, nr, sh.q, sh.pl[wid], Kh, kstride, Vh, vstride, scale_log2, mx, ls, o);
   }
+  float Mx[G], Ls[G];
+  lane_stats<G>(mx, ls, Mx, Ls);
   write_partial<G>(sh.o, sh.st, Mx, Ls, o, part + (size_t)blockIdx.x * G * (kHeadDim + 2));
 }
 
@@ -2300,10 +2326,10 @@ __global__ __launch_bounds__(kFusedThreads) __attribute__((amdgpu_waves_per_eu(f
     __syncthreads();
   }
   const int nrows = kept + extra;
-  float Mx[G], Ls[G], o[G][8];
+  float mx = -INFINITY, ls = 0.f;  // running (max, sum) of query head lane % 16 (lanes below G)
+  float o[G][8];
 #pragma unroll
   for (int g = 0; g < G; ++g) {
-    Mx[g] = -INFINITY, Ls[g] = 0.f;
 #pragma unroll
     for (int e = 0; e < 8; ++e) o[g][e] = 0.f;
   }
@@ -2324,7 +2350,7 @@ __global__ __launch_bounds__(kFusedThreads) __attribute__((amdgpu_waves_per_eu(f
       rv[1] = 4 * r4 + 1 < nr ? (uint32_t)v4.y : 0u;
       rv[2] = 4 * r4 + 2 < nr ? (uint32_t)v4.z : 0u;
       rv[3] = 4 * r4 + 3 < nr ? (uint32_t)v4.w : 0u;
-      attend_pass<G>(rk, rv, nr, sh.q, sh.pl[wid], Kh, kstride, Vh, vstride, scale_log2, Mx, Ls, o);
+      attend_pass<G>(rk, rv, nr, sh.q, sh.pl[wid], Kh, kstride, Vh, vstride, scale_log2, mx, ls, o);
     }
   } else {
     // more rows than the LDS list holds: rank r >= kRowCache is at
@@ -2363,7 +2389,7 @@ __global__ __launch_bounds__(kFusedThreads) __attribute__((amdgpu_waves_per_eu(f
       uint32_t rv[4];
 #pragma unroll
       for (int t = 0; t < 4; ++t) rv[t] = 4 * r4 + t < nr ? rank_row(q0 + 4 * r4 + t) : 0u;
-      attend_pass<G>(rk, rv, nr, sh.q, sh.pl[wid], Kh, kstride, Vh, vstride, scale_log2, Mx, Ls, o);
+      attend_pass<G>(rk, rv, nr, sh.q, sh.pl[wid], Kh, kstride, Vh, vstride, scale_log2, mx, ls, o);
     }
   }
   __syncthreads();  // the rows are read before the partial reuses their area
@@ -2371,6 +2397,8 @@ __global__ __launch_bounds__(kFusedThreads) __attribute__((amdgpu_waves_per_eu(f
 
   // ---- 5. the partial, published; the last slice of (b, h) merges -----
   float* my_part = part + sl * G * (kHeadDim + 2);
+  float Mx[G], Ls[G];
+  lane_stats<G>(mx, ls, Mx, Ls);
   write_partial<G, true>(sh.u.o, sh.st, Mx, Ls, o, my_part);
   stores_complete();
   __syncthreads();
