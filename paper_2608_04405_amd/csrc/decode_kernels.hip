@@ -793,7 +793,7 @@ __device__ __forceinline__ void attend_load_v(const uint32_t (&rv)[4], const cha
 
 template <int G>
 __device__ __forceinline__ void attend_logits(const uint4 (&kv)[4], int nrows, const uint4 (*qs)[kHeadDim / 8],
-                                              float (*pl)[16], float scale_log2, float& mx, float& ls, float& f);
+                                              float scale_log2, float& mx, float& ls, float& f, float (&x)[4]);
 template <int G>
 __device__ __forceinline__ void attend_pv(const uint4 (&vv)[4], float (*pl)[16], float f, float (&o)[G][8]);
 
@@ -806,8 +806,10 @@ __device__ __forceinline__ void attend_pass(uint32_t rk, const uint32_t (&rv)[4]
   uint4 kv[4], vv[4];
   attend_load_k(rk, Kh, kstride, kv);
   attend_load_v(rv, Vh, vstride, vv);
-  float f;
-  attend_logits<G>(kv, nrows, qs, pl, scale_log2, mx, ls, f);
+  float f, pr[4];
+  attend_logits<G>(kv, nrows, qs, scale_log2, mx, ls, f, pr);
+  if ((threadIdx.x & 15) < G)
+    *reinterpret_cast<float4*>(&pl[threadIdx.x & 15][4 * ((threadIdx.x & 63) >> 4)]) = make_float4(pr[0], pr[1], pr[2], pr[3]);
   attend_pv<G>(vv, pl, f, o);
 }
 
@@ -815,13 +817,13 @@ __device__ __forceinline__ void attend_pass(uint32_t rk, const uint32_t (&rv)[4]
 // computed in the lanes that hold them: lane (r, g) = (lane / 16, lane % 16),
 // g < G, has the logits of rows 4 r .. 4 r + 3 for query head g and keeps head
 // g's running maximum mx and sum ls (the same in its four row groups).  The
-// pass's probabilities go to the wavefront's LDS area pl; the rescale factor
-// of earlier passes comes back per head.  The arithmetic is that of a
+// pass's probabilities come back in x (zero in lanes g >= G), the rescale
+// factor of earlier passes in f.  The arithmetic is that of a
 // wavefront-uniform update: the maximum over the four row groups, then
 // exp2(logit - max), the group sums added as ((r0 + r1) + (r2 + r3)).
 template <int G>
 __device__ __forceinline__ void attend_logits(const uint4 (&kv)[4], int nrows, const uint4 (*qs)[kHeadDim / 8],
-                                              float (*pl)[16], float scale_log2, float& mx, float& ls, float& f) {
+                                              float scale_log2, float& mx, float& ls, float& f, float (&x)[4]) {
   static_assert(G <= 16, "the query heads of a group fill at most the 16 columns of a tile");
   const int lane = threadIdx.x & 63;
   const int c16 = lane & 15, r4 = lane >> 4;
@@ -835,7 +837,6 @@ __device__ __forceinline__ void attend_logits(const uint4 (&kv)[4], int nrows, c
     acc = mfma16(kv[kb].x, kv[kb].y, qv.x, qv.y, acc);
     acc = mfma16(kv[kb].z, kv[kb].w, qv.z, qv.w, acc);
   }
-  float x[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) x[j] = 4 * r4 + j < nrows ? acc[j] * scale_log2 : -INFINITY;
   // the pass's maximum over the 16 rows: the lane's four, then across the row groups
@@ -863,7 +864,9 @@ __device__ __forceinline__ void attend_logits(const uint4 (&kv)[4], int nrows, c
   }
   ls = ls * f + ps;
   mx = mnew;
-  if (c16 < G) *reinterpret_cast<float4*>(&pl[c16][4 * r4]) = make_float4(x[0], x[1], x[2], x[3]);
+  if (c16 >= G)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) x[j] = 0.f;
 }
 
 // The weighted V of the pass whose probabilities are in pl, after scaling
@@ -906,6 +909,89 @@ __device__ __forceinline__ void attend_pv(const uint4 (&vv)[4], float (*pl)[16],
   }
 }
 
+// The weighted V on the matrix cores.  D[head][dim] += P[head][row] V[row][dim]
+// for the pass's 16 rows is one 16 x 16 x 16 bf16 tile per 16 dims (heads
+// padded to 16 rows of D).  The A operand is the probabilities, which lane
+// (r, g) already holds for rows 4 r .. 4 r + 3 of head g, split into a bf16
+// high part and a bf16 low part (p - high), so the products keep about 16
+// significant bits of p and are accumulated in fp32 (two tiles per 16 dims).
+// The B operand wants, in lane (r, c), the four rows of dim 16 T + c: each
+// row group (16 lanes, rows 4 r .. 4 r + 3) stores its four V rows dim-major
+// ([dim][4 rows] bf16, 8 bytes per dim) in the wavefront's LDS area vt, and
+// every lane reads one 8-byte entry per tile.  Lane (r, c) accumulates
+// D[4 r + j][16 T + c] in acc[T][j].
+constexpr int kVtGroupBytes = kHeadDim * 8 + 16;  // one row group's block (padded: the groups start in other banks)
+constexpr int kVtWaveBytes = 4 * kVtGroupBytes;
+
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ uint32_t bf16x2_bits(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){a, b}, bf16x2_t));
+}
+
+template <int G>
+__device__ __forceinline__ void attend_pv_mfma(const uint4 (&vv)[4], const float (&pr)[4], float f, char* vt,
+                                               f32x4_t (&acc)[8]) {
+  const int lane = threadIdx.x & 63;
+  const int c16 = lane & 15, r4 = lane >> 4;
+  // rescale what earlier passes accumulated: D row j of this lane is head 4 r + j
+  if (__any(c16 < G && f != 1.f)) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const float fj = G <= 4 ? __int_as_float(__builtin_amdgcn_readlane(__float_as_int(f), j))
+                              : __shfl(f, 4 * r4 + j);
+#pragma unroll
+      for (int T = 0; T < 8; ++T) acc[T][j] *= fj;
+    }
+  }
+  // the row group's four rows, dim-major: dims 8 c + 2 m and 8 c + 2 m + 1 are
+  // the halves of word m of each row
+  char* grp = vt + r4 * kVtGroupBytes;
+#pragma unroll
+  for (int m = 0; m < 4; ++m) {
+    const uint32_t w0 = (&vv[0].x)[m], w1 = (&vv[1].x)[m], w2 = (&vv[2].x)[m], w3 = (&vv[3].x)[m];
+    uint4 d;
+    d.x = __builtin_amdgcn_perm(w1, w0, 0x05040100u);  // dim 2m: rows 0, 1
+    d.y = __builtin_amdgcn_perm(w3, w2, 0x05040100u);  //         rows 2, 3
+    d.z = __builtin_amdgcn_perm(w1, w0, 0x07060302u);  // dim 2m + 1: rows 0, 1
+    d.w = __builtin_amdgcn_perm(w3, w2, 0x07060302u);  //             rows 2, 3
+    *reinterpret_cast<uint4*>(grp + (8 * c16 + 2 * m) * 8) = d;
+  }
+  // the probabilities as bf16 high and low parts
+  const uint32_t h01 = bf16x2_bits(pr[0], pr[1]), h23 = bf16x2_bits(pr[2], pr[3]);
+  const uint32_t l01 = bf16x2_bits(pr[0] - __uint_as_float(h01 << 16), pr[1] - __uint_as_float(h01 & 0xFFFF0000u));
+  const uint32_t l23 = bf16x2_bits(pr[2] - __uint_as_float(h23 << 16), pr[3] - __uint_as_float(h23 & 0xFFFF0000u));
+  // LDS operations of one wavefront complete in order; the fences only keep
+  // the compiler from moving the reads above the writes
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+  for (int T = 0; T < 8; ++T) {
+    const uint2 bv = *reinterpret_cast<const uint2*>(grp + (16 * T + c16) * 8);
+    acc[T] = mfma16(h01, h23, bv.x, bv.y, acc[T]);
+    acc[T] = mfma16(l01, l23, bv.x, bv.y, acc[T]);
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();  // the next pass rewrites vt only after these reads
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// One pass with the weighted V on the matrix cores (see attend_pass).
+template <int G>
+__device__ __forceinline__ void attend_pass_mfma(uint32_t rk, const uint32_t (&rv)[4], int nrows,
+                                                 const uint4 (*qs)[kHeadDim / 8], char* vt, const char* Kh,
+                                                 uint32_t kstride, const char* Vh, uint32_t vstride, float scale_log2,
+                                                 float& mx, float& ls, f32x4_t (&acc)[8]) {
+  uint4 kv[4], vv[4];
+  attend_load_k(rk, Kh, kstride, kv);
+  attend_load_v(rv, Vh, vstride, vv);
+  float f, pr[4];
+  attend_logits<G>(kv, nrows, qs, scale_log2, mx, ls, f, pr);
+  attend_pv_mfma<G>(vv, pr, f, vt, acc);
+}
+
 // The running (max, sum) of each head as wavefront-uniform values, from the
 // lanes that hold them.
 template <int G>
@@ -939,6 +1025,10 @@ __device__ __forceinline__ uint64_t pub_load64(const uint64_t* p) {
 // weighted V over its four row groups; the wavefronts are combined under
 // their common maximum into pb[g] = (max, sum, o[128]) (base-2 logits).
 // o_s and st_s are LDS arrays; the caller ensures o_s is free to write.
+template <int G, bool PUBLISH>
+__device__ __forceinline__ void combine_partial(const float (&o_s)[kAttnWaves][G][kHeadDim],
+                                                const float (&st_s)[kAttnWaves][G][2], float* __restrict__ pb);
+
 template <int G, bool PUBLISH = false>  // PUBLISH: agent-scope atomic stores (read by the merging workgroup)
 __device__ __forceinline__ void write_partial(float (&o_s)[kAttnWaves][G][kHeadDim], float (&st_s)[kAttnWaves][G][2],
                                               const float (&Mx)[G], const float (&Ls)[G], float (&o)[G][8],
@@ -967,6 +1057,36 @@ __device__ __forceinline__ void write_partial(float (&o_s)[kAttnWaves][G][kHeadD
     for (int g = 0; g < G; ++g) st_s[wid][g][0] = Mx[g], st_s[wid][g][1] = Ls[g];
   }
   __syncthreads();
+  combine_partial<G, PUBLISH>(o_s, st_s, pb);
+}
+
+// write_partial for weighted V held as the matrix-core tiles of
+// attend_pv_mfma (already summed over the wavefront's rows).
+template <int G, bool PUBLISH = false>
+__device__ __forceinline__ void write_partial_tiles(float (&o_s)[kAttnWaves][G][kHeadDim],
+                                                    float (&st_s)[kAttnWaves][G][2], const float (&Mx)[G],
+                                                    const float (&Ls)[G], const f32x4_t (&acc)[8],
+                                                    float* __restrict__ pb) {
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const int c16 = lane & 15, r4 = lane >> 4;
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+    if (4 * r4 + j < G)
+#pragma unroll
+      for (int T = 0; T < 8; ++T) o_s[wid][4 * r4 + j][16 * T + c16] = acc[T][j];
+  if (lane == 0) {
+#pragma unroll
+    for (int g = 0; g < G; ++g) st_s[wid][g][0] = Mx[g], st_s[wid][g][1] = Ls[g];
+  }
+  __syncthreads();
+  combine_partial<G, PUBLISH>(o_s, st_s, pb);
+}
+
+// The wavefronts' partials, in o_s and st_s, combined under their common
+// maximum into pb[g] = (max, sum, o[128]).
+template <int G, bool PUBLISH>
+__device__ __forceinline__ void combine_partial(const float (&o_s)[kAttnWaves][G][kHeadDim],
+                                                const float (&st_s)[kAttnWaves][G][2], float* __restrict__ pb) {
   for (int e = threadIdx.x; e < G * (kHeadDim + 2); e += kAttnThreads) {
     const int g = e / (kHeadDim + 2), d = e % (kHeadDim + 2);
     float m = -INFINITY;
@@ -1646,6 +1766,9 @@ struct FusedShared {
 // waves per SIMD the kernel is built for: four 256-thread workgroups per CU
 // (the 1024-slice grid of a batch of 16 x 8 heads x 128K keys resident) where
 // LDS allows it; L = 128 holds 64 KB of histogram, so two
+static_assert(kVtWaveBytes * kFusedWaves <= (int)sizeof(uint32_t) * kWinSlices * kWinRec,
+              "the weighted-V transposes of the wavefronts fit in the window area");
+
 template <int L, int G>
 constexpr int fused_waves() { return L == 128 ? 2 : G <= 4 ? 4 : G == 8 ? 3 : 1; }
 
@@ -2327,12 +2450,10 @@ __global__ __launch_bounds__(kFusedThreads) __attribute__((amdgpu_waves_per_eu(f
   }
   const int nrows = kept + extra;
   float mx = -INFINITY, ls = 0.f;  // running (max, sum) of query head lane % 16 (lanes below G)
-  float o[G][8];
+  f32x4_t acc[8];
 #pragma unroll
-  for (int g = 0; g < G; ++g) {
-#pragma unroll
-    for (int e = 0; e < 8; ++e) o[g][e] = 0.f;
-  }
+  for (int T = 0; T < 8; ++T) acc[T] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  char* vt = reinterpret_cast<char*>(&sh.u.at.win[0][0]) + wid * kVtWaveBytes;  // free once T* is known
   const char* Kh = reinterpret_cast<const char*>(K + b * sK_b + h * sK_h);
   const char* Vh = reinterpret_cast<const char*>(V + b * sV_b + h * sV_h);
   const uint32_t kstride = (uint32_t)sK_n * 2u, vstride = (uint32_t)sV_n * 2u;
@@ -2350,7 +2471,7 @@ __global__ __launch_bounds__(kFusedThreads) __attribute__((amdgpu_waves_per_eu(f
       rv[1] = 4 * r4 + 1 < nr ? (uint32_t)v4.y : 0u;
       rv[2] = 4 * r4 + 2 < nr ? (uint32_t)v4.z : 0u;
       rv[3] = 4 * r4 + 3 < nr ? (uint32_t)v4.w : 0u;
-      attend_pass<G>(rk, rv, nr, sh.q, sh.pl[wid], Kh, kstride, Vh, vstride, scale_log2, mx, ls, o);
+      attend_pass_mfma<G>(rk, rv, nr, sh.q, vt, Kh, kstride, Vh, vstride, scale_log2, mx, ls, acc);
     }
   } else {
     // more rows than the LDS list holds: rank r >= kRowCache is at
@@ -2389,7 +2510,7 @@ __global__ __launch_bounds__(kFusedThreads) __attribute__((amdgpu_waves_per_eu(f
       uint32_t rv[4];
 #pragma unroll
       for (int t = 0; t < 4; ++t) rv[t] = 4 * r4 + t < nr ? rank_row(q0 + 4 * r4 + t) : 0u;
-      attend_pass<G>(rk, rv, nr, sh.q, sh.pl[wid], Kh, kstride, Vh, vstride, scale_log2, mx, ls, o);
+      attend_pass_mfma<G>(rk, rv, nr, sh.q, vt, Kh, kstride, Vh, vstride, scale_log2, mx, ls, acc);
     }
   }
   __syncthreads();  // the rows are read before the partial reuses their area
@@ -2399,7 +2520,7 @@ __global__ __launch_bounds__(kFusedThreads) __attribute__((amdgpu_waves_per_eu(f
   float* my_part = part + sl * G * (kHeadDim + 2);
   float Mx[G], Ls[G];
   lane_stats<G>(mx, ls, Mx, Ls);
-  write_partial<G, true>(sh.u.o, sh.st, Mx, Ls, o, my_part);
+  write_partial_tiles<G, true>(sh.u.o, sh.st, Mx, Ls, acc, my_part);
   stores_complete();
   __syncthreads();
   if (threadIdx.x == 0)

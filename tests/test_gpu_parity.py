@@ -142,7 +142,10 @@ def test_build_golden_worked_example():
     assert idx.cpu().numpy().ravel().tolist() == g["topk"]
     # softmax over keys 0 and 1 with logits 4/sqrt(128) and 0, values e0 and e1
     w0 = 1.0 / (1.0 + np.exp(-4.0 / np.sqrt(128)))
-    np.testing.assert_allclose(out.cpu().numpy()[0, 0, :2], [w0, 1 - w0], rtol=1e-6)
+    # the fused step weighs V on the matrix cores with each probability split
+    # into two bf16 parts (about 16 significant bits, relative error below
+    # 4e-6); the three-launch step keeps fp32 throughout
+    np.testing.assert_allclose(out.cpu().numpy()[0, 0, :2], [w0, 1 - w0], rtol=1e-5)
 
 
 # ------------------------------------------------------------------ Algorithm 2

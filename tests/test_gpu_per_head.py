@@ -97,7 +97,13 @@ def test_per_head_group_of_one_is_the_decode_step():
     idx_g = torch.empty(cfg.B, cfg.Hkv, cfg.k, dtype=torch.int32, device=DEV)
     out_g = bpc.decode_attention(d["q"], d["K"], d["V"], codes, P, cfg.k, idx_out=idx_g)
     torch.cuda.synchronize()
-    assert torch.equal(idx, idx_g) and torch.equal(out, out_g)
+    assert torch.equal(idx, idx_g)
+    if bpc.decode_path_taken(cfg.B, cfg.Hq, cfg.Hkv, cfg.N, cfg.L) == 1:
+        assert torch.equal(out, out_g)
+    else:
+        # the fused step sums the weighted V rows on the matrix cores (other
+        # rounding order), the per-head launches on the vector unit
+        assert torch.allclose(out, out_g, rtol=1e-5, atol=1e-6), (out - out_g).abs().max().item()
 
 
 def test_per_head_llama8b_ragged():
