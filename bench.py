@@ -220,13 +220,14 @@ def measure_config(bpc, cfg, dev, n_inst, steps, warmup, log_name):
     layers = cfg.layers
     n_data = layers if layers > 1 else n_inst
     frag = torch.zeros(1, dtype=torch.int64, device=dev)
+    fall = torch.zeros(1, dtype=torch.int64, device=dev)
     ws_build = torch.empty(bpc.build_workspace_bytes(B, Hkv, N, L), dtype=torch.uint8, device=dev)
-    build_ms = hash_ms = 0.0
+    build_ms = hash_ms = hash_mm_ms = 0.0
     data = []
     t0 = time.time()
     for i in range(n_data):
         d = make_layer(cfg, layer=i, device=dev)
-        ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
         ev[0].record()
         P, codes, _ = bpc.build_hash(d["K"], d["G"].to(dev), fragile=frag if i == 0 or layers > 1 else None,
                                      workspace=ws_build)
@@ -234,11 +235,17 @@ def measure_config(bpc, cfg, dev, n_inst, steps, warmup, log_name):
         if i == 0 or layers > 1:
             c2, _ = bpc.hash_keys(d["K"], P)
         ev[2].record()
+        if i == 0 or layers > 1:
+            c3 = bpc.hash_keys_mm(d["K"], P, fallbacks=fall)
+        ev[3].record()
         torch.cuda.synchronize()
         if i == 0 or layers > 1:
             build_ms += ev[0].elapsed_time(ev[1])
             hash_ms += ev[1].elapsed_time(ev[2])
-            del c2
+            hash_mm_ms += ev[2].elapsed_time(ev[3])
+            if not torch.equal(c2, c3):
+                raise RuntimeError(f"{log_name}: matrix-core Algorithm 2 codes differ from the fp64 kernel's")
+            del c2, c3
         data.append({"q": d["q"], "K": d["K"], "V": d["V"], "codes": codes, "P": P})
         del d
     del ws_build
@@ -270,6 +277,8 @@ def measure_config(bpc, cfg, dev, n_inst, steps, warmup, log_name):
            "decode_path": "fused single launch" if bpc.decode_path_taken(B, Hq, Hkv, N, L) == 0 else "three launches",
            "prefill": {"build_ms": round(build_ms, 2), "hash_ms": round(hash_ms, 2),
                        "build_keys_per_s": keys_pf / (build_ms * 1e-3), "hash_keys_per_s": keys_pf / (hash_ms * 1e-3),
+                       "hash_mm_ms": round(hash_mm_ms, 2), "hash_mm_keys_per_s": keys_pf / (hash_mm_ms * 1e-3),
+                       "hash_mm_recomputed_decisions": int(fall.item()),
                        "fragile_sign_decisions": int(frag.item()),
                        "covers": "all layers" if layers > 1 else "one instance"}}
     log(f"{log_name}: {res['us_per_step']} us/step, {res['keys_per_s']:.3g} keys/s, {res['hbm_frac'] * 100:.1f} % of "
@@ -330,29 +339,47 @@ def main():
     prefill = {}
     frag = torch.zeros(1, dtype=torch.int64, device=dev)
     frag2 = torch.zeros(1, dtype=torch.int64, device=dev)
+    frag3 = torch.zeros(1, dtype=torch.int64, device=dev)
+    fall3 = torch.zeros(1, dtype=torch.int64, device=dev)
     for i, it in enumerate(insts):
-        ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
         ev[0].record()
         err = torch.empty(B, Hkv, N, dtype=torch.float32, device=dev)
         P, codes, _ = bpc.build_hash(it["K"], it["G"], err_out=err, fragile=frag if i == 0 else None,
                                      workspace=ws_build)
         ev[1].record()
         if i == 0 and not args.no_prefill:
-            codes2, _ = bpc.hash_keys(it["K"], P, fragile=frag2)
-        ev[2].record()
+            err2 = torch.empty(B, Hkv, N, dtype=torch.float32, device=dev)
+            codes2, _ = bpc.hash_keys(it["K"], P, err_out=err2, fragile=frag2)
+            ev[2].record()
+            codes3 = bpc.hash_keys_mm(it["K"], P, fragile=frag3, fallbacks=fall3)
+            ev[3].record()
+            codes4, _ = bpc.hash_keys(it["K"], P)
+            ev[4].record()
         torch.cuda.synchronize()
         it["P"], it["codes"], it["err"] = P, codes, err
         if i == 0 and not args.no_prefill:
             build_ms = ev[0].elapsed_time(ev[1])
             hash_ms = ev[1].elapsed_time(ev[2])
+            hash_mm_ms = ev[2].elapsed_time(ev[3])
+            hash_codes_ms = ev[3].elapsed_time(ev[4])
+            if not (torch.equal(codes2, codes3) and torch.equal(codes2, codes4)) or int(frag2.item()) != int(frag3.item()):
+                raise RuntimeError("matrix-core Algorithm 2 differs from the fp64 kernel")
             keys = B * Hkv * N
             prefill = {"build_ms": round(build_ms, 3), "hash_ms": round(hash_ms, 3),
                        "build_keys_per_s": keys / (build_ms / 1e3), "hash_keys_per_s": keys / (hash_ms / 1e3),
+                       "hash_codes_only_ms": round(hash_codes_ms, 3),
+                       "hash_mm_ms": round(hash_mm_ms, 3), "hash_mm_keys_per_s": keys / (hash_mm_ms / 1e3),
+                       "hash_mm_speedup": round(hash_codes_ms / hash_mm_ms, 2),
+                       "hash_mm_recomputed_decisions": int(fall3.item()),
                        "fragile_sign_decisions_build": int(frag.item()),
                        "fragile_sign_decisions_hash": int(frag2.item()),
-                       "what": "Algorithm 1 (build P and codes) and Algorithm 2 (hash every key) for the whole "
-                               "batch, fp64 fixed-order arithmetic; fragile = sign decisions with |a| < 1e-6"}
-            del codes2
+                       "what": "Algorithm 1 (build P, codes and errors) and Algorithm 2 (hash every key, with "
+                               "errors) for the whole batch, fp64 fixed-order arithmetic; hash_codes_only: the same "
+                               "kernel without the errors; hash_mm: the same codes with the projections on the "
+                               "matrix cores and certified signs (recomputed = decisions redone in fp64); fragile = "
+                               "sign decisions with |a| < 1e-6"}
+            del codes2, codes3, codes4, err2
     del ws_build
     torch.cuda.empty_cache()
     log(f"prefill {prefill}")
@@ -503,7 +530,7 @@ def main():
             ev[0].record()
             Pcal = bpc.build_hash(Kcal, insts[0]["G"])[0][0]
             ev[1].record()
-            codes_opc, _ = bpc.hash_keys(insts[0]["K"], Pcal)
+            codes_opc = bpc.hash_keys_mm(insts[0]["K"], Pcal)
             ev[2].record()
             torch.cuda.synchronize()
             del Kcal
@@ -514,7 +541,7 @@ def main():
                    "prefill_hash_ms": round(ev[1].elapsed_time(ev[2]), 3),
                    "decode_us_per_step_same_instance": round(opc_us, 2),
                    "what": "P per KV head from Algorithm 1 over 131072 held-out keys; prefill = Algorithm 2 of the "
-                           "whole batch against it; decode with the shared P, one instance repeated (its data "
+                           "whole batch against it (matrix-core path); decode with the shared P, one instance repeated (its data "
                            "partly stays in the 256 MB last-level cache)"}
             del codes_opc
             log(f"offline calibration: {opc}")

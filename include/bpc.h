@@ -163,6 +163,32 @@ int bpc_hash_keys(const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t sK_n,
                   void* stream);
 
 /*
+ * bpc_hash_keys_mm -- the codes of bpc_hash_keys, bit for bit, and the same
+ * fragile count, with the projections on the matrix cores (Algorithm "Given
+ * projection, computing hashcode"; App. "CUDA Optimizations on Bitwise
+ * Operations", hashing kernel).  Unrolling the residual of Algorithm 2
+ * gives a_i = k . P_i - sum_{t<i} u_t (P_t . P_i): the products k . P_i are
+ * one dense contraction (bf16 MFMA on P cut exactly into three bf16 parts,
+ * fp32 accumulation), the sum over earlier bits uses the Gram matrix of P in
+ * fp32.  Each sign is kept only when |a^| exceeds a bound on its distance to
+ * the fixed-order fp64 value of bpc_hash_keys (plus the fragile threshold);
+ * every other decision is recomputed in that fixed-order arithmetic.
+ *
+ * Arguments as for bpc_hash_keys, without err_out (residual norms need the
+ * fp64 residual itself: use bpc_hash_keys for them).
+ * fallbacks_out  device uint64 accumulator (or NULL): decisions recomputed
+ *            in the fixed-order arithmetic.
+ * No workspace; one kernel launch.
+ */
+int bpc_hash_keys_mm(const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t sK_n,
+                     int B, int Hkv, int N, int D, int L,
+                     const float* P, int64_t sP_b, int64_t sP_h,
+                     uint32_t* codes_out, int64_t sC_b, int64_t sC_h,
+                     unsigned long long* fragile_out,
+                     unsigned long long* fallbacks_out,
+                     void* stream);
+
+/*
  * bpc_append_kv -- decode-time append of T new tokens to the cache: their
  * key and value rows are stored at positions [pos, pos + T) of K and V, and
  * each new key is hashed against the given projection with the iterative

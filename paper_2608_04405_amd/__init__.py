@@ -23,6 +23,7 @@ __all__ = [
     "build_hash",
     "build_workspace_bytes",
     "hash_keys",
+    "hash_keys_mm",
     "decode_attention",
     "decode_workspace_bytes",
     "decode_attention_per_head",
@@ -61,6 +62,8 @@ _lib.bpc_build_hash.restype = _i
 _lib.bpc_build_hash.argtypes = [_p, _i64, _i64, _i64, _i, _i, _i, _i, _i, _p, _p, _p, _i64, _i64, _p, _p, _p, _sz, _p]
 _lib.bpc_hash_keys.restype = _i
 _lib.bpc_hash_keys.argtypes = [_p, _i64, _i64, _i64, _i, _i, _i, _i, _i, _p, _i64, _i64, _p, _i64, _i64, _p, _p, _p]
+_lib.bpc_hash_keys_mm.restype = _i
+_lib.bpc_hash_keys_mm.argtypes = [_p, _i64, _i64, _i64, _i, _i, _i, _i, _i, _p, _i64, _i64, _p, _i64, _i64, _p, _p, _p]
 _lib.bpc_decode_workspace_bytes.restype = _sz
 _lib.bpc_decode_workspace_bytes.argtypes = [_i, _i, _i, _i, _i, _i, _i]
 _DECODE_ARGS = [_p, _p, _i64, _i64, _i64, _p, _i64, _i64, _i64, _p, _i64, _i64, _p, _i64, _i64,
@@ -331,6 +334,34 @@ def hash_keys(K: torch.Tensor, P: torch.Tensor, N: Optional[int] = None, *,
                               _stream(stream)),
            "bpc_hash_keys")
     return codes_out, err_out
+
+
+def hash_keys_mm(K: torch.Tensor, P: torch.Tensor, N: Optional[int] = None, *,
+                 codes_out: Optional[torch.Tensor] = None, fragile: Optional[torch.Tensor] = None,
+                 fallbacks: Optional[torch.Tensor] = None, stream=None):
+    """The codes of hash_keys (Algorithm 2), bit for bit, with the
+    projections on the matrix cores and certified signs.  fragile and
+    fallbacks are device uint64 accumulators ([1] int64 tensors).  Returns
+    codes."""
+    _need(K, "K", torch.bfloat16, 4)
+    B, Hkv, Ncap, D = K.shape
+    N = Ncap if N is None else N
+    if not 1 <= N <= Ncap:
+        raise ValueError(f"N={N} must satisfy 1 <= N <= {Ncap}")
+    L, sPb, sPh = _proj(P, D, B, Hkv)
+    if codes_out is not None:
+        _u32_codes(codes_out, "codes_out")
+        _extent(codes_out, "codes_out", (B, Hkv, ("ge", N), L // 32))
+    _fragile(fragile)
+    _fragile(fallbacks)
+    _on_gpu(K, P, codes_out, fragile, fallbacks)
+    if codes_out is None:
+        codes_out = torch.zeros(B, Hkv, Ncap, L // 32, dtype=torch.int32, device=K.device)
+    _check(_lib.bpc_hash_keys_mm(_ptr(K), *_kv_strides(K), B, Hkv, N, D, L, _ptr(P), sPb, sPh, _ptr(codes_out),
+                                 codes_out.stride(0), codes_out.stride(1), _ptr(fragile), _ptr(fallbacks),
+                                 _stream(stream)),
+           "bpc_hash_keys_mm")
+    return codes_out
 
 
 def _decode_inputs(q, K, V, codes, P, k, N):

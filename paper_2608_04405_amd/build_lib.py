@@ -23,7 +23,7 @@ CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libbpc.so")
 OUT_TRACE = os.path.join(HERE, "libbpc_trace.so")
 BUILD_DIR = os.path.join(os.path.dirname(HERE), "_build")
-SOURCES = ["bpc_api.hip", "build_kernels.hip", "decode_kernels.hip", "eas_kernels.hip"]
+SOURCES = ["bpc_api.hip", "build_kernels.hip", "decode_kernels.hip", "eas_kernels.hip", "hash_mm_kernels.hip"]
 ARCH = os.environ.get("BPC_OFFLOAD_ARCH", "gfx950")
 
 COMMON = [

@@ -209,6 +209,23 @@ int bpc_hash_keys(const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t sK_n, i
   return BPC_OK;
 }
 
+int bpc_hash_keys_mm(const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t sK_n, int B, int Hkv, int N, int D,
+                     int L, const float* P, int64_t sP_b, int64_t sP_h, uint32_t* codes_out, int64_t sC_b,
+                     int64_t sC_h, unsigned long long* fragile_out, unsigned long long* fallbacks_out, void* stream) {
+  g_last_error[0] = 0;
+  int st;
+  if ((st = check_sizes(B, Hkv, N))) return st;
+  if ((st = check_head_dim(D))) return st;
+  if ((st = check_code_len(L))) return st;
+  if ((st = check_kv("K", K, sK_b, sK_h, sK_n))) return st;
+  if ((st = check_proj(P, sP_b, sP_h))) return st;
+  if ((st = check_codes("codes_out", codes_out, sC_b, sC_h, L / 32))) return st;
+  hipError_t e = launch_hash_mm(K, sK_b, sK_h, sK_n, B, Hkv, N, L, P, sP_b, sP_h, codes_out, sC_b, sC_h, fragile_out,
+                                fallbacks_out, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "bpc_hash_keys_mm launch");
+  return BPC_OK;
+}
+
 int bpc_append_kv(const uint16_t* k_new, int64_t sKn_b, int64_t sKn_h, int64_t sKn_t, const uint16_t* v_new,
                   int64_t sVn_b, int64_t sVn_h, int64_t sVn_t, uint16_t* K, int64_t sK_b, int64_t sK_h,
                   int64_t sK_n, uint16_t* V, int64_t sV_b, int64_t sV_h, int64_t sV_n, uint32_t* codes,

@@ -168,6 +168,12 @@ hipError_t launch_hash(const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t sK
                        int64_t sC_b, int64_t sC_h, float* err, unsigned long long* fragile,
                        hipStream_t stream, const AppendCopy* append = nullptr);
 
+// Algorithm 2 with the projections on the matrix cores and certified signs
+// (codes and fragile count identical to launch_hash; no residual norms).
+hipError_t launch_hash_mm(const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t sK_n, int B, int Hkv, int N, int L,
+                          const float* P, int64_t sP_b, int64_t sP_h, uint32_t* codes, int64_t sC_b, int64_t sC_h,
+                          unsigned long long* fragile, unsigned long long* fallbacks, hipStream_t stream);
+
 hipError_t launch_build(const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t sK_n, int B, int Hkv,
                         int N, int L, const float* G, float* P, uint32_t* codes, int64_t sC_b,
                         int64_t sC_h, float* err, unsigned long long* fragile, char* ws,

@@ -144,6 +144,27 @@ def test_hash_rejects(lib, kw, code):
     assert _hash(lib, **kw) == code
 
 
+def _hash_mm(lib, **kw):
+    a = dict(K=FAKE, sKb=0, sKh=4096 * 128, sKn=128, B=1, Hkv=8, N=4096, D=128, L=64, P=FAKE, sPb=0, sPh=0,
+             codes=FAKE, sCb=8 * 4096 * 2, sCh=4096 * 2, frag=None, fall=None, stream=None)
+    a.update(kw)
+    f = lib.bpc_hash_keys_mm
+    f.restype = ctypes.c_int
+    return f(ctypes.c_void_p(a["K"]), _i64(a["sKb"]), _i64(a["sKh"]), _i64(a["sKn"]), a["B"], a["Hkv"], a["N"],
+             a["D"], a["L"], ctypes.c_void_p(a["P"]), _i64(a["sPb"]), _i64(a["sPh"]), ctypes.c_void_p(a["codes"]),
+             _i64(a["sCb"]), _i64(a["sCh"]), ctypes.c_void_p(a["frag"]), ctypes.c_void_p(a["fall"]),
+             ctypes.c_void_p(a["stream"]))
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(K=None), EINVAL), (dict(P=None), EINVAL), (dict(codes=None), EINVAL), (dict(N=0), EINVAL),
+    (dict(B=0), EINVAL), (dict(L=96), EUNSUP), (dict(D=64), EUNSUP), (dict(sCh=4096 * 2 + 1), EALIGN),
+    (dict(P=FAKE + 4), EALIGN), (dict(K=FAKE + 2), EALIGN), (dict(sKn=100), EINVAL), (dict(sPh=-4), EINVAL),
+])
+def test_hash_mm_rejects(lib, kw, code):
+    assert _hash_mm(lib, **kw) == code
+
+
 def _build(lib, **kw):
     a = dict(K=FAKE, sKb=0, sKh=4096 * 128, sKn=128, B=1, Hkv=8, N=4096, D=128, L=32, G=FAKE, P=FAKE,
              codes=FAKE, sCb=8 * 4096, sCh=4096, err=None, frag=None, ws=FAKE, ws_bytes=0, stream=None)

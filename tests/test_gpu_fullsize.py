@@ -189,6 +189,16 @@ def check_hash(cfg, d, P, rec, label):
     assert sha(u32(c2[0, 0, :cfg.N])) == rec["hash"]["codes"], f"{label}: Algorithm 2 codes differ"
     assert sha(err[0, 0].cpu().numpy()) == rec["hash"]["err_f32"], f"{label}: Algorithm 2 errors differ"
     assert int(frag.item()) == rec["hash"]["fragile"], f"{label}: Algorithm 2 fragile count differs"
+    # the matrix-core path with certified signs: the same codes and count
+    frag.zero_()
+    fall = torch.zeros(1, dtype=torch.int64, device=DEV)
+    c3 = bpc.hash_keys_mm(d["K"][b:b + 1, h:h + 1], P[b:b + 1, h:h + 1].contiguous(), N=cfg.N, fragile=frag,
+                          fallbacks=fall)
+    torch.cuda.synchronize()
+    assert sha(u32(c3[0, 0, :cfg.N])) == rec["hash"]["codes"], f"{label}: matrix-core Algorithm 2 codes differ"
+    assert int(frag.item()) == rec["hash"]["fragile"], f"{label}: matrix-core fragile count differs"
+    announce(f"{label}: matrix-core Algorithm 2 bit-exact, {int(fall.item())} of {cfg.N * cfg.L} decisions "
+             f"recomputed in fp64")
 
 
 def check_variants(cfg, d, P, codes, err, rec, label):
