@@ -80,12 +80,24 @@ int bpc_version(void);
  * bpc_set_decode_path -- how the decode entry points run a step, for this
  * process: 0 (the default) runs it as one fused launch whenever every
  * workgroup of the step fits on the current device at once, else as three
- * launches; 1 always uses the three launches (for comparisons and tests).
- * Calls already enqueued are not affected; workspace sizes follow the path
- * (bpc_decode_workspace_bytes queries it).  Returns BPC_EINVAL for any other
- * value.
+ * launches; the fused launch splits each (b, h) into slices of 16384 keys,
+ * or of 4096 or 8192 keys (code lengths 32 and 64, groups of up to 8 query
+ * heads) when those still fit, at most two workgroups per compute unit, and
+ * the larger slices would leave most of the device idle.  1 always uses the three
+ * launches, 2 the fused launch on 16384-key slices only (both for
+ * comparisons and tests).  Calls already enqueued are not affected;
+ * workspace sizes follow the path (bpc_decode_workspace_bytes queries it).
+ * Returns BPC_EINVAL for any other value.
  */
 int bpc_set_decode_path(int path);
+
+/*
+ * bpc_decode_slice_keys -- keys per slice (16384, 8192 or 4096) a decode step of
+ * this shape would use on the current device under the current setting (the
+ * three-launch path always uses 16384); shapes the decode entry points
+ * reject return 0.
+ */
+int bpc_decode_slice_keys(int B, int Hq, int Hkv, int N, int L);
 
 /*
  * bpc_decode_path_taken -- which path a decode step of this shape would take

@@ -37,6 +37,7 @@ __all__ = [
     "version",
     "set_decode_path",
     "decode_path_taken",
+    "decode_slice_keys",
     "DECODE_ZEROED_BYTES",
 ]
 
@@ -90,6 +91,8 @@ _lib.bpc_select_hard.restype = _i
 _lib.bpc_select_hard.argtypes = [_p, _i64, _i64, _i, _i, _i, _i, _p, _p]
 _lib.bpc_set_decode_path.restype = _i
 _lib.bpc_set_decode_path.argtypes = [_i]
+_lib.bpc_decode_slice_keys.restype = _i
+_lib.bpc_decode_slice_keys.argtypes = [_i, _i, _i, _i, _i]
 _lib.bpc_decode_path_taken.restype = _i
 _lib.bpc_decode_path_taken.argtypes = [_i, _i, _i, _i, _i]
 _lib.bpc_decode_noalloc_max_bytes.restype = _sz
@@ -125,7 +128,9 @@ def version() -> int:
 
 def set_decode_path(path: int) -> None:
     """0: a decode step runs as one fused launch whenever its workgroups fit
-    on the GPU at once (the default); 1: always the three launches."""
+    on the GPU at once (the default; 4096- or 8192-key slices where
+    16384-key ones would leave the GPU mostly idle); 1: always the three
+    launches; 2: the fused launch on 16384-key slices only."""
     _check(_lib.bpc_set_decode_path(int(path)), "bpc_set_decode_path")
 
 
@@ -133,6 +138,12 @@ def decode_path_taken(B: int, Hq: int, Hkv: int, N: int, L: int) -> int:
     """0 if a decode step of this shape runs as one fused launch on the
     current device, 1 if as three launches (needs a GPU)."""
     return int(_lib.bpc_decode_path_taken(B, Hq, Hkv, N, L))
+
+
+def decode_slice_keys(B: int, Hq: int, Hkv: int, N: int, L: int) -> int:
+    """Keys per slice (16384, 8192 or 4096) of a decode step of this shape on the
+    current device (needs a GPU)."""
+    return int(_lib.bpc_decode_slice_keys(B, Hq, Hkv, N, L))
 
 
 def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:

@@ -79,8 +79,10 @@ DecodeLayout decode_layout(int B, int Hq, int Hkv, int N, int L, int k) {
   const size_t BH = (size_t)B * Hkv;
   d.W = L / 32;
   d.G = Hq / Hkv;
-  d.nslices = (N + kSlice - 1) / kSlice;
-  d.fused = decode_fused_ok(B, Hq, Hkv, N, L);
+  const int fused_slice = decode_fused_slice(B, Hq, Hkv, N, L);
+  d.fused = fused_slice != 0;
+  d.slice = d.fused ? fused_slice : kSlice;
+  d.nslices = (N + d.slice - 1) / d.slice;
   const size_t S = BH * d.nslices;
   size_t o = 0;
   auto take = [&](size_t bytes) {
@@ -151,9 +153,16 @@ const char* bpc_last_error(void) { return g_last_error; }
 int bpc_version(void) { return 200; }
 
 int bpc_set_decode_path(int path) {
-  if (path != 0 && path != 1) return fail(BPC_EINVAL, "path=%d must be 0 (automatic) or 1 (three launches)", path);
+  if (path < 0 || path > 2)
+    return fail(BPC_EINVAL, "path=%d must be 0 (automatic), 1 (three launches) or 2 (fused, large slices only)", path);
   decode_set_path(path);
   return BPC_OK;
+}
+
+int bpc_decode_slice_keys(int B, int Hq, int Hkv, int N, int L) {
+  if (B < 1 || Hq < 1 || Hkv < 1 || N < 1 || (L != 32 && L != 64 && L != 128)) return 0;
+  const int sl = decode_fused_slice(B, Hq, Hkv, N, L);
+  return sl ? sl : kSlice;
 }
 
 int bpc_decode_path_taken(int B, int Hq, int Hkv, int N, int L) {

@@ -19,6 +19,11 @@ constexpr int kHeadDim = 128;
 // (sequence, KV head); the slice's distances stay in registers and its
 // histogram in LDS.  At most kMaxSlices slices per (sequence, KV head).
 constexpr int kSlice = 16384;
+// The fused decode path also runs on slices of 8192 or 4096 keys when the
+// kSlice grid would leave most of the device idle (code lengths 32 and 64,
+// groups of up to 8 query heads).
+constexpr int kSliceMid = 8192;
+constexpr int kSliceSmall = 4096;
 constexpr int kScoreThreads = 512;  // scoring workgroup: 32 keys per thread
 constexpr int kMaxSlices = 1024;
 // One attention workgroup per slice keeps its selected candidates, read in
@@ -88,6 +93,7 @@ constexpr int kQcodeStride = 64;
 // [B Hkv][k] int32.
 struct DecodeLayout {
   bool fused;
+  int slice;  // keys per slice (kSlice, or kSliceMid / kSliceSmall on the fused path)
   int nslices, G, W;
   size_t off_cand, off_meta, off_hist_fine, off_hist_cc, off_win, off_part, off_qcode, total;
   size_t off_sync, off_pub, off_rows;
@@ -99,10 +105,12 @@ struct BuildLayout {
 };
 
 DecodeLayout decode_layout(int B, int Hq, int Hkv, int N, int L, int k);
-// Whether the current device runs the decode step as the single fused
-// launch: every slice's workgroup must be resident at once.
-bool decode_fused_ok(int B, int Hq, int Hkv, int N, int L);
-// 0: automatic; 1: always the three-launch path
+// Keys per slice when the current device runs the decode step as the single
+// fused launch (every slice's workgroup resident at once), else 0.
+int decode_fused_slice(int B, int Hq, int Hkv, int N, int L);
+inline bool decode_fused_ok(int B, int Hq, int Hkv, int N, int L) { return decode_fused_slice(B, Hq, Hkv, N, L) != 0; }
+// 0: automatic; 1: always the three-launch path; 2: the fused path only on
+// slices of kSlice keys (for comparisons)
 void decode_set_path(int path);
 BuildLayout build_layout(int B, int Hkv, int N, int L);
 

@@ -1772,7 +1772,7 @@ static_assert(kVtWaveBytes * kFusedWaves <= (int)sizeof(uint32_t) * kWinSlices *
 template <int L, int G>
 constexpr int fused_waves() { return L == 128 ? 2 : G <= 4 ? 4 : G == 8 ? 3 : 1; }
 
-template <int L, int G>
+template <int L, int G, int SL>
 __global__ __launch_bounds__(kFusedThreads) __attribute__((amdgpu_waves_per_eu(fused_waves<L, G>()))) void fused_decode_kernel(
     const uint16_t* __restrict__ q, const float* __restrict__ P, int64_t sP_b, int64_t sP_h,
     const uint32_t* __restrict__ codes, int64_t sC_b, int64_t sC_h, const uint16_t* __restrict__ K, int64_t sK_b,
@@ -1786,19 +1786,19 @@ __global__ __launch_bounds__(kFusedThreads) __attribute__((amdgpu_waves_per_eu(f
   constexpr int NW = kFusedWaves;
   constexpr int NB = FusedShared<L, G>::NB;
   constexpr int NBP = FusedShared<L, G>::NBP;
-  constexpr int PER = kSlice / NT;       // keys per thread
+  constexpr int PER = SL / NT;          // keys per thread
   constexpr int KPL = 4 / W;             // keys per 16-byte load
   constexpr int NLD = PER / KPL;         // loads per thread
   constexpr int RD = kFusedRing < NLD ? kFusedRing : NLD;
-  constexpr int KPW = kSlice / NW;       // keys per wavefront: a contiguous run
+  constexpr int KPW = SL / NW;          // keys per wavefront: a contiguous run
   constexpr int KSTEP = 64 * KPL;        // keys per load of the wavefront
   __shared__ FusedShared<L, G> sh;
 
   int bh, s;
   slice_tile(blockIdx.x, BH, nslices, bh, s);
   const int b = bh / Hkv, h = bh % Hkv;
-  const int n0 = s * kSlice;
-  const int cnt = min(kSlice, N - n0);
+  const int n0 = s * SL;
+  const int cnt = min(SL, N - n0);
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   const size_t sl = (size_t)bh * nslices + s;
   uint32_t* my_pub = pub + sl * kPubStride;
@@ -1808,7 +1808,7 @@ __global__ __launch_bounds__(kFusedThreads) __attribute__((amdgpu_waves_per_eu(f
 
   // ---- 1. query packing and scoring -----------------------------------
   const uint32_t* cb = codes + b * sC_b + h * sC_h + (int64_t)n0 * W;
-  const bool full = cnt == kSlice && (reinterpret_cast<uintptr_t>(cb) & 15u) == 0;
+  const bool full = cnt == SL && (reinterpret_cast<uintptr_t>(cb) & 15u) == 0;
   auto key_of = [&](int it, int u) -> int { return wid * KPW + it * KSTEP + lane * KPL + u; };
   auto load_group = [&](int r) -> u32x4_t {
     const int n = key_of(r, 0);
@@ -2300,7 +2300,7 @@ __global__ __launch_bounds__(kFusedThreads) __attribute__((amdgpu_waves_per_eu(f
   // the selection reads the candidate list only; otherwise the slice's keys
   // are walked again from the registers.
   if (m > 0)
-    for (int i = threadIdx.x; i < kSlice / 32; i += NT) sh.u.at.sel[i] = 0u;
+    for (int i = threadIdx.x; i < SL / 32; i += NT) sh.u.at.sel[i] = 0u;
   int32_t* grow = rows + (size_t)bh * k;  // the (b, h)'s global row list (ranks past the LDS list)
   const bool from_cands = by_window && ncand <= kRowCache;
   if (from_cands) {
@@ -2694,7 +2694,7 @@ static int device_cu_count() {
   return c;
 }
 
-template <int L, int G>
+template <int L, int G, int SL>
 static int fused_capacity() {
   constexpr int kDevices = 64;
   static std::atomic<int> cap[kDevices];
@@ -2703,7 +2703,7 @@ static int fused_capacity() {
   int c = cap[dev].load();
   if (c == 0) {
     int nb = 0, ncu = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, fused_decode_kernel<L, G>, kFusedThreads, 0) != hipSuccess ||
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, fused_decode_kernel<L, G, SL>, kFusedThreads, 0) != hipSuccess ||
         hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
       return 0;  // (the error is reported by the launch path)
     c = max(nb * ncu, 0) + 1;  // stored + 1 so that 0 means "not queried"
@@ -2712,27 +2712,70 @@ static int fused_capacity() {
   return c - 1;
 }
 
-template <int L>
+template <int L, int SL>
 static int fused_capacity_L(int G) {
   switch (G) {
-    case 1: return fused_capacity<L, 1>();
-    case 2: return fused_capacity<L, 2>();
-    case 4: return fused_capacity<L, 4>();
-    case 8: return fused_capacity<L, 8>();
-    case 16: return fused_capacity<L, 16>();
+    case 1: return fused_capacity<L, 1, SL>();
+    case 2: return fused_capacity<L, 2, SL>();
+    case 4: return fused_capacity<L, 4, SL>();
+    case 8: return fused_capacity<L, 8, SL>();
+    case 16: return fused_capacity<L, 16, SL>();
     default: return 0;
   }
 }
 
-bool decode_fused_ok(int B, int Hq, int Hkv, int N, int L) {
-  if (g_decode_path.load() == 1 || Hkv < 1 || Hq % Hkv || (int64_t)B * Hkv > kFusedMaxBH) return false;
-  const int G = Hq / Hkv;
-  const int64_t nwg = (int64_t)B * Hkv * ((N + kSlice - 1) / kSlice);
-  const int cap = L == 32 ? fused_capacity_L<32>(G) : L == 64 ? fused_capacity_L<64>(G) : fused_capacity_L<128>(G);
-  return nwg <= cap;
+// the small-slice instances: code lengths 32 and 64, groups of up to 8
+static bool small_slices_built(int L, int G) { return L != 128 && G <= 8; }
+
+template <int SL>
+static int fused_capacity_small(int L, int G) {
+  if (!small_slices_built(L, G)) return 0;
+  if (L == 32) {
+    switch (G) {
+      case 1: return fused_capacity<32, 1, SL>();
+      case 2: return fused_capacity<32, 2, SL>();
+      case 4: return fused_capacity<32, 4, SL>();
+      default: return fused_capacity<32, 8, SL>();
+    }
+  }
+  switch (G) {
+    case 1: return fused_capacity<64, 1, SL>();
+    case 2: return fused_capacity<64, 2, SL>();
+    case 4: return fused_capacity<64, 4, SL>();
+    default: return fused_capacity<64, 8, SL>();
+  }
 }
 
-template <int L>
+static int fused_capacity_of(int L, int G, int SL) {
+  if (SL == kSliceSmall) return fused_capacity_small<kSliceSmall>(L, G);
+  if (SL == kSliceMid) return fused_capacity_small<kSliceMid>(L, G);
+  if (SL != kSlice) return 0;
+  return L == 32 ? fused_capacity_L<32, kSlice>(G) : L == 64 ? fused_capacity_L<64, kSlice>(G) : fused_capacity_L<128, kSlice>(G);
+}
+
+int decode_fused_slice(int B, int Hq, int Hkv, int N, int L) {
+  const int path = g_decode_path.load();
+  if (path == 1 || Hkv < 1 || Hq % Hkv || (int64_t)B * Hkv > kFusedMaxBH) return 0;
+  const int G = Hq / Hkv;
+  // Smaller slices where the 16384-key grid leaves the device mostly idle:
+  // the smallest size whose grid stays within two workgroups per compute
+  // unit (measured: batch 8 x 8 heads x 65536 keys 37.8 -> 34.7 us on 8192
+  // keys, 40.9 on 4096; batch 1 x 8 heads x 32768 keys 35.4 -> 25.3 us on
+  // 4096), fits on the device at once and keeps each (b, h) within the
+  // one-round threshold's 64 slices.
+  if (path == 0 && small_slices_built(L, G)) {
+    const int64_t ncu = device_cu_count();
+    for (const int sl : {kSliceSmall, kSliceMid}) {
+      const int64_t ns = (N + sl - 1) / sl;
+      const int64_t nwg = (int64_t)B * Hkv * ns;
+      if (ns > 1 && ns <= kWinSlices && nwg <= 2 * ncu && nwg <= fused_capacity_of(L, G, sl)) return sl;
+    }
+  }
+  const int64_t nwg = (int64_t)B * Hkv * ((N + kSlice - 1) / kSlice);
+  return nwg <= fused_capacity_of(L, G, kSlice) ? kSlice : 0;
+}
+
+template <int L, int SL>
 static hipError_t launch_fused_L(const DecodeArgs& a, const DecodeLayout& lay) {
   const int BH = a.B * a.Hkv;
   const int nwg = BH * lay.nslices;
@@ -2750,10 +2793,11 @@ static hipError_t launch_fused_L(const DecodeArgs& a, const DecodeLayout& lay) {
   switch (lay.G) {
 #define BPC_FUSED_CASE(GG)                                                                                          \
   case GG:                                                                                                          \
-    fused_decode_kernel<L, GG><<<nwg, kFusedThreads, 0, st>>>(                                                      \
-        a.q, a.P, a.sP_b, a.sP_h, a.codes, a.sC_b, a.sC_h, a.K, a.sK_b, a.sK_h, a.sK_n, a.V, a.sV_b, a.sV_h, a.sV_n, \
-        BH, a.Hkv, a.N, a.k, lay.nslices, scale_log2, sync, pub, part, rows, a.out, a.idx_out, a.score_out,          \
-        a.qcode_out, a.serr, a.sS_b, a.sS_h, a.m, a.added_out, ncu);                                                 \
+    if constexpr (SL == kSlice || GG <= 8)                                                                          \
+      fused_decode_kernel<L, GG, SL><<<nwg, kFusedThreads, 0, st>>>(                                                \
+          a.q, a.P, a.sP_b, a.sP_h, a.codes, a.sC_b, a.sC_h, a.K, a.sK_b, a.sK_h, a.sK_n, a.V, a.sV_b, a.sV_h,      \
+          a.sV_n, BH, a.Hkv, a.N, a.k, lay.nslices, scale_log2, sync, pub, part, rows, a.out, a.idx_out,            \
+          a.score_out, a.qcode_out, a.serr, a.sS_b, a.sS_h, a.m, a.added_out, ncu);                                  \
     break;
     BPC_FUSED_CASE(1)
     BPC_FUSED_CASE(2)
@@ -2772,10 +2816,12 @@ static hipError_t launch_fused_L(const DecodeArgs& a, const DecodeLayout& lay) {
 
 hipError_t launch_decode(const DecodeArgs& a, const DecodeLayout& lay) {
   if (lay.fused) {
+    if (lay.slice == kSliceSmall) return a.L == 32 ? launch_fused_L<32, kSliceSmall>(a, lay) : launch_fused_L<64, kSliceSmall>(a, lay);
+    if (lay.slice == kSliceMid) return a.L == 32 ? launch_fused_L<32, kSliceMid>(a, lay) : launch_fused_L<64, kSliceMid>(a, lay);
     switch (a.L) {
-      case 32: return launch_fused_L<32>(a, lay);
-      case 64: return launch_fused_L<64>(a, lay);
-      default: return launch_fused_L<128>(a, lay);
+      case 32: return launch_fused_L<32, kSlice>(a, lay);
+      case 64: return launch_fused_L<64, kSlice>(a, lay);
+      default: return launch_fused_L<128, kSlice>(a, lay);
     }
   }
   switch (a.L) {

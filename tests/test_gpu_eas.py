@@ -29,12 +29,13 @@ else:  # pragma: no cover
 
 DEV = "cuda"
 
-@pytest.fixture(autouse=True, params=["fused", "three-launch"])
+@pytest.fixture(autouse=True, params=["fused", "fused-16k", "three-launch"])
 def decode_path(request):
-    """Every test here runs on both decode paths: the single fused launch
-    (the default wherever the step's workgroups fit on the GPU at once) and
-    the three launches (the path for larger steps)."""
-    bpc.set_decode_path(0 if request.param == "fused" else 1)
+    """Every test here runs on each decode path: the single fused launch
+    (the default wherever the step's workgroups fit on the GPU at once, on
+    4096-key slices where those fit), the fused launch on 16384-key slices
+    only, and the three launches (the path for larger steps)."""
+    bpc.set_decode_path({"fused": 0, "fused-16k": 2, "three-launch": 1}[request.param])
     yield request.param
     bpc.set_decode_path(0)
 
