@@ -2540,10 +2540,60 @@ __global__ __launch_bounds__(kFusedThreads) __attribute__((amdgpu_waves_per_eu(f
               (uint32_t)(nslices - 1);
   __syncthreads();
   if (!sh.flag) return;
-  // the merge: every slice's (max, sum) per query head into LDS, then one
-  // output coordinate per thread and step
   const float* pbh = part + (size_t)bh * nslices * G * (kHeadDim + 2);
   const size_t cstride = (size_t)G * (kHeadDim + 2);
+  if (L != 32 && nslices <= 64) {
+    // The merge, up to 64 slices (and L >= 64: at L = 32 the extra registers
+    // spill elsewhere in the kernel): per query head (one wavefront, lane u =
+    // slice u) the common maximum, each slice's weight exp2(max_u - M) and
+    // the weighted sum of the slices' sums (a butterfly, the same in every
+    // lane); then each thread one pair of output coordinates, summed over
+    // the slices in ascending order with every load of a batch in flight.
+    float* wts = reinterpret_cast<float*>(&sh.u.hist[0]);  // [64][G] weights, then [G] totals
+    float* tot = wts + 64 * G;
+    for (int g = wid; g < G; g += NW) {
+      float m = -INFINITY, l = 0.f;
+      if (lane < nslices) {
+        const uint64_t v =
+            pub_load64(reinterpret_cast<const uint64_t*>(pbh + (size_t)lane * cstride + (size_t)g * (kHeadDim + 2)));
+        m = __uint_as_float((uint32_t)v), l = __uint_as_float((uint32_t)(v >> 32));
+      }
+      float M = m;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) M = fmaxf(M, __shfl_xor(M, o, 64));
+      const float w = (m == -INFINITY) ? 0.f : exp2f(m - M);
+      float sum = w * l;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) sum += __shfl_xor(sum, o, 64);
+      wts[lane * G + g] = w;
+      if (lane == 0) tot[g] = sum;
+    }
+    __syncthreads();
+    for (int e = threadIdx.x; e < G * (kHeadDim / 2); e += NT) {
+      const int g = e / (kHeadDim / 2), d2 = e % (kHeadDim / 2);
+      const float* pg = pbh + (size_t)g * (kHeadDim + 2) + 2 + 2 * d2;
+      float a0 = 0.f, a1 = 0.f;
+      constexpr int MB = 16;  // loads in flight
+      for (int u0 = 0; u0 < nslices; u0 += MB) {
+        uint64_t v[MB];
+#pragma unroll
+        for (int j = 0; j < MB; ++j)
+          v[j] = (u0 + j < nslices) ? pub_load64(reinterpret_cast<const uint64_t*>(pg + (size_t)(u0 + j) * cstride)) : 0u;
+#pragma unroll
+        for (int j = 0; j < MB; ++j)
+          if (u0 + j < nslices) {
+            const float w = wts[(u0 + j) * G + g];
+            a0 = fmaf(w, __uint_as_float((uint32_t)v[j]), a0);
+            a1 = fmaf(w, __uint_as_float((uint32_t)(v[j] >> 32)), a1);
+          }
+      }
+      float* op = out + ((size_t)b * Hkv * G + (size_t)h * G + g) * kHeadDim + 2 * d2;
+      op[0] = a0 / tot[g];
+      op[1] = a1 / tot[g];
+    }
+  } else
+  // the merge, more than 64 slices: every slice's (max, sum) per query head
+  // with each output coordinate, rescaled batch by batch of eight slices
   for (int e = threadIdx.x; e < G * kHeadDim; e += NT) {
     const int g = e / kHeadDim, d = e % kHeadDim;
     float Mg = -INFINITY, lsum = 0.f, acc = 0.f;
