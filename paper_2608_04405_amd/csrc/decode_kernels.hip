@@ -1712,14 +1712,16 @@ __device__ __forceinline__ int sum_published(int nslices, Addr addr, F f) {
 }
 // Copy nv published words, word e from src(e), to dst[e] in LDS; R loads per
 // thread are in flight before the first is used.
-template <int R, class Src>
-__device__ __forceinline__ void copy_published(uint32_t* dst, int nv, Src src) {
+template <int R, class T, class Src>
+__device__ __forceinline__ void copy_published(T* dst, int nv, Src src) {
   for (int e0 = 0; e0 < nv; e0 += R * kFusedThreads) {
-    uint32_t v[R];
+    T v[R];
 #pragma unroll
     for (int r = 0; r < R; ++r) {
       const int e = e0 + (int)threadIdx.x + r * kFusedThreads;
-      v[r] = (e < nv) ? pub_load(src(e)) : 0u;
+      v[r] = (e < nv) ? T(sizeof(T) == 8 ? pub_load64(reinterpret_cast<const uint64_t*>(src(e)))
+                                         : pub_load(reinterpret_cast<const uint32_t*>(src(e))))
+                      : T(0);
     }
     // the values are taken here, so that the compiler cannot sink each load
     // into the conditional store that uses it (and wait on them one by one)
@@ -2150,14 +2152,20 @@ __global__ __launch_bounds__(kFusedThreads) __attribute__((amdgpu_waves_per_eu(f
   bool planned = false, by_window = false;
   if (arrived && nslices <= kWinSlices) {
     // one round over the window records (see the attention kernel above)
-    const int nv = nslices * kWinRec;
-    auto src = [&](int e) { return bh_pub + (size_t)(e / kWinRec) * kPubStride + e % kWinRec; };
-    if (nv <= 2 * NT)
-      copy_published<2>(&sh.u.at.win[0][0], nv, src);
-    else if (nv <= 4 * NT)
-      copy_published<4>(&sh.u.at.win[0][0], nv, src);
+    // (as 64-bit words: a record is kWinRec / 2 of them, 8-byte aligned)
+    constexpr int RW = kWinRec / 2;
+    static_assert(kWinRec % 2 == 0 && kPubStride % 2 == 0, "records of whole 64-bit words");
+    const int nv = nslices * RW;
+    uint64_t* wdst = reinterpret_cast<uint64_t*>(&sh.u.at.win[0][0]);
+    auto src = [&](int e) {
+      return reinterpret_cast<const uint64_t*>(bh_pub + (size_t)(e / RW) * kPubStride) + e % RW;
+    };
+    if (nv <= NT)
+      copy_published<1>(wdst, nv, src);
+    else if (nv <= 2 * NT)
+      copy_published<2>(wdst, nv, src);
     else
-      copy_published<(kWinSlices * kWinRec + NT - 1) / NT>(&sh.u.at.win[0][0], nv, src);
+      copy_published<(kWinSlices * RW + NT - 1) / NT>(wdst, nv, src);
     __syncthreads();
     auto cum = [&](int u, int t) -> int {  // base_u - 1 <= t < base_u + kWinBins
       const int j = t - (int)sh.u.at.win[u][0];
