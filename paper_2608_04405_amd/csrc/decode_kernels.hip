@@ -2082,11 +2082,13 @@ __global__ __launch_bounds__(kFusedThreads) __attribute__((amdgpu_waves_per_eu(f
     }
     for (int c = threadIdx.x; c <= kCoarseBins; c += NT) pub_store(my_pub + kPubCoarse + c, sh.cc[c]);
   }
+  BPC_STAMP(1, 5);
   // arrival: every published store of the workgroup is complete first (and
   // every read of the histogram, whose area holds the candidates next)
   stores_complete();
   __syncthreads();
   if (threadIdx.x == 0) __hip_atomic_fetch_add(bh_sync + 0, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  BPC_STAMP(1, 7);
   // While the other slices finish: the candidates (distance <= cand_max) in
   // key order into the LDS list (at most kRowCache of them).  In key order a
   // lane's KPL keys of one load follow those of the lanes below it: each
@@ -2152,6 +2154,8 @@ __global__ __launch_bounds__(kFusedThreads) __attribute__((amdgpu_waves_per_eu(f
   bool planned = false, by_window = false;
   if (arrived && nslices <= kWinSlices) {
     // one round over the window records (see the attention kernel above)
+    static_assert(2 * kCoarseBins >= kWinBins + 1 && kWinBins + 1 <= 3 * 64, "S(t) fits the scratch and three lanes");
+    if (threadIdx.x < 2 * kCoarseBins) (&sh.gsum[0][0])[threadIdx.x] = 0;  // S(t) below (after the copy's barrier)
     // (as 64-bit words: a record is kWinRec / 2 of them, 8-byte aligned)
     constexpr int RW = kWinRec / 2;
     static_assert(kWinRec % 2 == 0 && kPubStride % 2 == 0, "records of whole 64-bit words");
@@ -2167,6 +2171,7 @@ __global__ __launch_bounds__(kFusedThreads) __attribute__((amdgpu_waves_per_eu(f
     else
       copy_published<(kWinSlices * RW + NT - 1) / NT>(wdst, nv, src);
     __syncthreads();
+    BPC_NOTE(1, 12, __builtin_amdgcn_s_memrealtime());
     auto cum = [&](int u, int t) -> int {  // base_u - 1 <= t < base_u + kWinBins
       const int j = t - (int)sh.u.at.win[u][0];
       const uint32_t w = sh.u.at.win[u][4 + (max(j, 0) >> 1)];
@@ -2174,12 +2179,44 @@ __global__ __launch_bounds__(kFusedThreads) __attribute__((amdgpu_waves_per_eu(f
     };
     const int lo = wave_reduce_maxmin<true>(lane < nslices ? (int)sh.u.at.win[lane][0] : 0);
     const int hi = wave_reduce_maxmin<false>(lane < nslices ? (int)sh.u.at.win[lane][1] : (1 << 30));
+    // S(t) = sum over the slices of cum_u(t) for t = lo - 1 + i, i < span
+    // (at most kWinBins + 1 values): wavefront w adds up slices w, w + NW,
+    // ...; lane l holds i = l, l + 64, l + 128, and the wavefronts' sums meet
+    // in LDS through atomic adds (integers: the order does not matter).
+    // (One thread per t summing every slice waited on two dependent LDS
+    // reads per slice: 6.5 us with 64 slices.)
+    int* Ssum = &sh.gsum[0][0];
+    const int span = lo <= hi ? hi - lo + 2 : 0;
+    if (lo <= hi) {
+      int a0 = 0, a1 = 0, a2 = 0;
+      // the bases and below-window counts of the wavefront's slices, lane v
+      // holding slice wid + NW v: read once, then taken by read-lane, so that
+      // no LDS read waits on another
+      const int uv = wid + NW * lane;
+      const int vbase = uv < nslices ? (int)sh.u.at.win[uv][0] : 0;
+      const int vbelow = uv < nslices ? (int)sh.u.at.win[uv][2] : 0;
+      int v = 0;
+#pragma unroll 4
+      for (int u = wid; u < nslices; u += NW, ++v) {
+        const int base = __builtin_amdgcn_readlane(vbase, v), blw = __builtin_amdgcn_readlane(vbelow, v);
+        auto val = [&](int i) -> int {  // cum_u(lo - 1 + i)
+          const int j = lo - 1 + i - base;
+          const uint32_t w = sh.u.at.win[u][4 + (max(j, 0) >> 1)];
+          return j < 0 ? blw : (int)((j & 1) ? (w >> 16) : (w & 0xFFFFu));
+        };
+        a0 += lane < span ? val(lane) : 0;
+        a1 += lane + 64 < span ? val(lane + 64) : 0;
+        a2 += lane + 128 < span ? val(lane + 128) : 0;
+      }
+      if (lane < span) atomicAdd(&Ssum[lane], a0);
+      if (lane + 64 < span) atomicAdd(&Ssum[lane + 64], a1);
+      if (lane + 128 < span) atomicAdd(&Ssum[lane + 128], a2);
+    }
+    __syncthreads();
     bool below = false, badt = false;
     const int t = lo - 1 + (int)threadIdx.x;
     if (lo <= hi && t <= hi) {
-      int St = 0;
-#pragma unroll 8
-      for (int u = 0; u < nslices; ++u) St += cum(u, t);
+      const int St = Ssum[threadIdx.x];
       if (t == lo - 1)
         badt = St >= k;
       else
@@ -2189,6 +2226,7 @@ __global__ __launch_bounds__(kFusedThreads) __attribute__((amdgpu_waves_per_eu(f
     const unsigned long long mbelow = __ballot(below), mbad = __ballot(badt);
     if (lane == 0) sh.red[0][wid] = (int)__popcll(mbelow), sh.red[1][wid] = mbad != 0ull;
     __syncthreads();
+    BPC_NOTE(1, 13, __builtin_amdgcn_s_memrealtime());
     int cntlow = 0, bad = lo > hi;
 #pragma unroll
     for (int w = 0; w < NW; ++w) cntlow += sh.red[0][w], bad |= sh.red[1][w];
@@ -2300,6 +2338,7 @@ __global__ __launch_bounds__(kFusedThreads) __attribute__((amdgpu_waves_per_eu(f
   if (!planned) kept = 0;  // a bounded wait ran out: this slice contributes nothing
   kept = max(0, min(kept, k - off));
   BPC_STAMP(1, 4);
+  BPC_NOTE(1, 14, by_window ? 1 : 2);
 
   // ---- 4. selection and attention -----------------------------------
   // A kept key's rank among the slice's kept keys (key order) is (keys below
