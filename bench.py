@@ -275,6 +275,7 @@ def measure_config(bpc, cfg, dev, n_inst, steps, warmup, log_name):
            "keys_per_s": keys / (us * 1e-6), "token_positions_per_s": B * N * layers / (us * 1e-6),
            "step_algorithmic_bytes": nbytes, "hbm_frac": round(nbytes / (us * 1e-6) / (HBM_PEAK_GBS * 1e9), 4),
            "decode_path": "fused single launch" if bpc.decode_path_taken(B, Hq, Hkv, N, L) == 0 else "three launches",
+           "slice_keys": bpc.decode_slice_keys(B, Hq, Hkv, N, L),
            "prefill": {"build_ms": round(build_ms, 2), "hash_ms": round(hash_ms, 2),
                        "build_keys_per_s": keys_pf / (build_ms * 1e-3), "hash_keys_per_s": keys_pf / (hash_ms * 1e-3),
                        "hash_mm_ms": round(hash_mm_ms, 2), "hash_mm_keys_per_s": keys_pf / (hash_mm_ms * 1e-3),
@@ -607,7 +608,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": cfg.name, "B": B, "Hq": Hq, "Hkv": Hkv, "head_dim": D, "N": N, "code_bits": L,
                    "k": k, "budget": "2%", "instances": args.instances,
-                   "decode_path": "fused single launch" if fused else "three launches"},
+                   "decode_path": "fused single launch" if fused else "three launches",
+                   "slice_keys": bpc.decode_slice_keys(B, Hq, Hkv, N, L)},
         "runs_us_per_step": [round(x, 2) for x in runs],
         "median_us_per_step": round(float(np.median(runs)), 2),
         "mean_us_per_step": round(float(np.mean(runs)), 2),
