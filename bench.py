@@ -222,12 +222,13 @@ def measure_config(bpc, cfg, dev, n_inst, steps, warmup, log_name):
     frag = torch.zeros(1, dtype=torch.int64, device=dev)
     fall = torch.zeros(1, dtype=torch.int64, device=dev)
     ws_build = torch.empty(bpc.build_workspace_bytes(B, Hkv, N, L), dtype=torch.uint8, device=dev)
-    build_ms = hash_ms = hash_mm_ms = 0.0
+    ws_ck = torch.empty(bpc.build_checkpoint_workspace_bytes(B, Hkv, N, L), dtype=torch.uint8, device=dev)
+    build_ms = build_ck_ms = hash_ms = hash_mm_ms = 0.0
     data = []
     t0 = time.time()
     for i in range(n_data):
         d = make_layer(cfg, layer=i, device=dev)
-        ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
         ev[0].record()
         P, codes, _ = bpc.build_hash(d["K"], d["G"].to(dev), fragile=frag if i == 0 or layers > 1 else None,
                                      workspace=ws_build)
@@ -238,17 +239,23 @@ def measure_config(bpc, cfg, dev, n_inst, steps, warmup, log_name):
         if i == 0 or layers > 1:
             c3 = bpc.hash_keys_mm(d["K"], P, fallbacks=fall)
         ev[3].record()
+        if i == 0 or layers > 1:
+            P4, c4, _ = bpc.build_hash(d["K"], d["G"].to(dev), workspace=ws_ck)
+        ev[4].record()
         torch.cuda.synchronize()
         if i == 0 or layers > 1:
             build_ms += ev[0].elapsed_time(ev[1])
             hash_ms += ev[1].elapsed_time(ev[2])
             hash_mm_ms += ev[2].elapsed_time(ev[3])
+            build_ck_ms += ev[3].elapsed_time(ev[4])
             if not torch.equal(c2, c3):
                 raise RuntimeError(f"{log_name}: matrix-core Algorithm 2 codes differ from the fp64 kernel's")
-            del c2, c3
+            if not (torch.equal(P4, P) and torch.equal(c4, codes)):
+                raise RuntimeError(f"{log_name}: the checkpointed Algorithm 1 build differs from the recomputing one")
+            del c2, c3, P4, c4
         data.append({"q": d["q"], "K": d["K"], "V": d["V"], "codes": codes, "P": P})
         del d
-    del ws_build
+    del ws_build, ws_ck
     torch.cuda.empty_cache()
     keys_pf = B * Hkv * N * (layers if layers > 1 else 1)
     log(f"{log_name}: {n_data} layers/instances generated and built in {time.time() - t0:.1f}s")
@@ -278,6 +285,7 @@ def measure_config(bpc, cfg, dev, n_inst, steps, warmup, log_name):
            "slice_keys": bpc.decode_slice_keys(B, Hq, Hkv, N, L),
            "prefill": {"build_ms": round(build_ms, 2), "hash_ms": round(hash_ms, 2),
                        "build_keys_per_s": keys_pf / (build_ms * 1e-3), "hash_keys_per_s": keys_pf / (hash_ms * 1e-3),
+                       "build_checkpoint_ms": round(build_ck_ms, 2),
                        "hash_mm_ms": round(hash_mm_ms, 2), "hash_mm_keys_per_s": keys_pf / (hash_mm_ms * 1e-3),
                        "hash_mm_recomputed_decisions": int(fall.item()),
                        "fragile_sign_decisions": int(frag.item()),
@@ -357,6 +365,15 @@ def main():
             ev[3].record()
             codes4, _ = bpc.hash_keys(it["K"], P)
             ev[4].record()
+            # Algorithm 1 again, keeping the fp64 residual every 16 bits
+            del ws_build
+            ws_ck = torch.empty(bpc.build_checkpoint_workspace_bytes(B, Hkv, N, L), dtype=torch.uint8, device=dev)
+            err5 = torch.empty(B, Hkv, N, dtype=torch.float32, device=dev)
+            frag5 = torch.zeros(1, dtype=torch.int64, device=dev)
+            ev5 = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+            ev5[0].record()
+            P5, codes5, _ = bpc.build_hash(it["K"], it["G"], err_out=err5, fragile=frag5, workspace=ws_ck)
+            ev5[1].record()
         torch.cuda.synchronize()
         it["P"], it["codes"], it["err"] = P, codes, err
         if i == 0 and not args.no_prefill:
@@ -364,11 +381,17 @@ def main():
             hash_ms = ev[1].elapsed_time(ev[2])
             hash_mm_ms = ev[2].elapsed_time(ev[3])
             hash_codes_ms = ev[3].elapsed_time(ev[4])
+            build_ck_ms = ev5[0].elapsed_time(ev5[1])
             if not (torch.equal(codes2, codes3) and torch.equal(codes2, codes4)) or int(frag2.item()) != int(frag3.item()):
                 raise RuntimeError("matrix-core Algorithm 2 differs from the fp64 kernel")
+            if not (torch.equal(P5, P) and torch.equal(codes5, codes) and torch.equal(err5, err)
+                    and int(frag5.item()) == int(frag.item())):
+                raise RuntimeError("the checkpointed Algorithm 1 build differs from the recomputing one")
             keys = B * Hkv * N
             prefill = {"build_ms": round(build_ms, 3), "hash_ms": round(hash_ms, 3),
                        "build_keys_per_s": keys / (build_ms / 1e3), "hash_keys_per_s": keys / (hash_ms / 1e3),
+                       "build_checkpoint_ms": round(build_ck_ms, 3),
+                       "build_checkpoint_workspace_bytes": int(ws_ck.numel()),
                        "hash_codes_only_ms": round(hash_codes_ms, 3),
                        "hash_mm_ms": round(hash_mm_ms, 3), "hash_mm_keys_per_s": keys / (hash_mm_ms / 1e3),
                        "hash_mm_speedup": round(hash_codes_ms / hash_mm_ms, 2),
@@ -376,11 +399,13 @@ def main():
                        "fragile_sign_decisions_build": int(frag.item()),
                        "fragile_sign_decisions_hash": int(frag2.item()),
                        "what": "Algorithm 1 (build P, codes and errors) and Algorithm 2 (hash every key, with "
-                               "errors) for the whole batch, fp64 fixed-order arithmetic; hash_codes_only: the same "
+                               "errors) for the whole batch, fp64 fixed-order arithmetic; build_checkpoint: the same "
+                               "build keeping each key's fp64 residual every 16 bits (same results); hash_codes_only: the same "
                                "kernel without the errors; hash_mm: the same codes with the projections on the "
                                "matrix cores and certified signs (recomputed = decisions redone in fp64); fragile = "
                                "sign decisions with |a| < 1e-6"}
-            del codes2, codes3, codes4, err2
+            del codes2, codes3, codes4, err2, ws_ck, P5, codes5, err5
+            ws_build = None
     del ws_build
     torch.cuda.empty_cache()
     log(f"prefill {prefill}")

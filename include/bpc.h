@@ -134,13 +134,19 @@ int bpc_decode_path_taken(int B, int Hq, int Hkv, int N, int L);
  *           decisions is ADDED (the caller zeroes it), or NULL
  * workspace    device memory of at least bpc_build_workspace_bytes(...)
  *           bytes, 256-byte aligned; its contents on entry do not matter.
- * Cost: 2 L + 2 kernel launches.  Nothing of size N x D is stored: each
- * bit's pass recomputes R_j from the bf16 key, the key's code bits so far
- * and P (the same rounded subtractions, in the same order), so the
- * workspace holds one fp64 partial sum per 128-key chunk and coordinate
- * plus fp64 copies of P and G.
+ * Cost: 2 L + 2 kernel launches.  With that workspace nothing of size N x D
+ * is stored: each bit's pass recomputes R_j from the bf16 key, the key's
+ * code bits so far and P (the same rounded subtractions, in the same
+ * order), so the workspace holds one fp64 partial sum per 128-key chunk
+ * and coordinate plus fp64 copies of P and G.  Given at least
+ * bpc_build_checkpoint_workspace_bytes(...) bytes (1 KiB more per key,
+ * rounded up to 128-key chunks), the build also keeps each key's fp64
+ * residual there every 16 bits and later passes start from it, trading
+ * that memory and its traffic for fewer recomputed subtractions; the
+ * results are bit for bit the same.
  */
 size_t bpc_build_workspace_bytes(int B, int Hkv, int N, int D, int L);
+size_t bpc_build_checkpoint_workspace_bytes(int B, int Hkv, int N, int D, int L);
 int bpc_build_hash(const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t sK_n,
                    int B, int Hkv, int N, int D, int L,
                    const float* G,

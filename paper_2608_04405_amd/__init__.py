@@ -22,6 +22,7 @@ __all__ = [
     "LIB_PATH",
     "build_hash",
     "build_workspace_bytes",
+    "build_checkpoint_workspace_bytes",
     "hash_keys",
     "hash_keys_mm",
     "decode_attention",
@@ -59,6 +60,8 @@ _lib.bpc_last_error.argtypes = []
 _lib.bpc_version.restype = _i
 _lib.bpc_build_workspace_bytes.restype = _sz
 _lib.bpc_build_workspace_bytes.argtypes = [_i, _i, _i, _i, _i]
+_lib.bpc_build_checkpoint_workspace_bytes.restype = _sz
+_lib.bpc_build_checkpoint_workspace_bytes.argtypes = [_i, _i, _i, _i, _i]
 _lib.bpc_build_hash.restype = _i
 _lib.bpc_build_hash.argtypes = [_p, _i64, _i64, _i64, _i, _i, _i, _i, _i, _p, _p, _p, _i64, _i64, _p, _p, _p, _sz, _p]
 _lib.bpc_hash_keys.restype = _i
@@ -250,6 +253,10 @@ def build_workspace_bytes(B: int, Hkv: int, N: int, L: int, D: int = 128) -> int
     return int(_lib.bpc_build_workspace_bytes(B, Hkv, N, D, L))
 
 
+def build_checkpoint_workspace_bytes(B: int, Hkv: int, N: int, L: int, D: int = 128) -> int:
+    return int(_lib.bpc_build_checkpoint_workspace_bytes(B, Hkv, N, D, L))
+
+
 def decode_workspace_bytes(B: int, Hq: int, Hkv: int, N: int, L: int, k: int, D: int = 128) -> int:
     return int(_lib.bpc_decode_workspace_bytes(B, Hq, Hkv, N, D, L, k))
 
@@ -276,14 +283,16 @@ def _fragile(fragile: Optional[torch.Tensor]) -> None:
 def build_hash(K: torch.Tensor, G: torch.Tensor, N: Optional[int] = None, *,
                P_out: Optional[torch.Tensor] = None, codes_out: Optional[torch.Tensor] = None,
                err_out: Optional[torch.Tensor] = None, fragile: Optional[torch.Tensor] = None,
-               workspace: Optional[torch.Tensor] = None, stream=None):
+               workspace: Optional[torch.Tensor] = None, checkpoint: bool = False, stream=None):
     """Binary principal components of every (b, h): returns (P, codes, err).
 
     K [B, Hkv, >=N, 128] bf16; G [L, 128] fp32 Gaussian directions.  codes
     are int32 storage [B, Hkv, Ncap, L/32] holding the packed bits; err_out,
     when given, is a contiguous [B, Hkv, N] fp32 tensor.  When `fragile` (a
     1-element int64 GPU tensor) is given, the number of fragile sign
-    decisions is added to it."""
+    decisions is added to it.  With `checkpoint` the workspace allocated
+    here also holds the fp64 residual checkpoint (1 KiB per key); a given
+    workspace enables it by its size alone.  Results are the same."""
     _need(K, "K", torch.bfloat16, 4)
     B, Hkv, Ncap, D = K.shape
     N = Ncap if N is None else N
@@ -309,7 +318,7 @@ def build_hash(K: torch.Tensor, G: torch.Tensor, N: Optional[int] = None, *,
         P_out = torch.empty(B, Hkv, L, D, dtype=torch.float32, device=dev)
     if codes_out is None:
         codes_out = torch.zeros(B, Hkv, Ncap, W, dtype=torch.int32, device=dev)
-    ws_bytes = build_workspace_bytes(B, Hkv, N, L, D)
+    ws_bytes = (build_checkpoint_workspace_bytes if checkpoint else build_workspace_bytes)(B, Hkv, N, L, D)
     if workspace is None:
         workspace = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
     _check(_lib.bpc_build_hash(_ptr(K), *_kv_strides(K), B, Hkv, N, D, L, _ptr(G), _ptr(P_out),

@@ -121,6 +121,9 @@ BuildLayout build_layout(int B, int Hkv, int N, int L) {
   b.off_g64 = o;   // G widened to fp64
   o = align_up(o + (size_t)L * kHeadDim * sizeof(double), 256);
   b.total = o;
+  b.off_ck = o;    // fp64 residual of every key, padded to whole chunks
+  o = align_up(o + BH * b.nchunks * (size_t)kBuildChunk * kHeadDim * sizeof(double), 256);
+  b.total_ck = o;
   return b;
 }
 
@@ -175,6 +178,11 @@ size_t bpc_build_workspace_bytes(int B, int Hkv, int N, int D, int L) {
   return build_layout(B, Hkv, N, L).total;
 }
 
+size_t bpc_build_checkpoint_workspace_bytes(int B, int Hkv, int N, int D, int L) {
+  if (B < 1 || Hkv < 1 || N < 1 || D != kHeadDim) return 0;
+  return build_layout(B, Hkv, N, L).total_ck;
+}
+
 int bpc_build_hash(const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t sK_n, int B, int Hkv, int N,
                    int D, int L, const float* G, float* P_out, uint32_t* codes_out, int64_t sC_b,
                    int64_t sC_h, float* err_out, unsigned long long* fragile_out, void* workspace,
@@ -194,8 +202,10 @@ int bpc_build_hash(const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t sK_n, 
     return fail(BPC_EWORKSPACE, "workspace of %zu bytes given, %zu needed", workspace ? workspace_bytes : 0,
                 lay.total);
   if (reinterpret_cast<uintptr_t>(workspace) & 255u) return fail(BPC_EALIGN, "workspace must be 256-byte aligned");
+  const bool checkpoint = workspace_bytes >= lay.total_ck;
   hipError_t e = launch_build(K, sK_b, sK_h, sK_n, B, Hkv, N, L, G, P_out, codes_out, sC_b, sC_h, err_out,
-                              fragile_out, static_cast<char*>(workspace), static_cast<hipStream_t>(stream));
+                              fragile_out, static_cast<char*>(workspace), checkpoint,
+                              static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "bpc_build_hash launch");
   return BPC_OK;
 }

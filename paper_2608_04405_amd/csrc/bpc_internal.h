@@ -73,6 +73,11 @@ constexpr size_t kSyncRegionBytes = kSyncCounterBytes + (size_t)kFusedMaxBH * kF
 constexpr int kBuildGroups = 2;                  // groups of 64 keys per build workgroup
 constexpr int kBuildThreads = 256 * kBuildGroups;  // four wavefronts (coordinate blocks) per group
 constexpr int kBuildChunk = 64 * kBuildGroups;     // keys per workgroup (one chunk of the row tree)
+#ifndef BPC_BUILD_CKPT_PERIOD
+#define BPC_BUILD_CKPT_PERIOD 16
+#endif
+// bits between stored fp64 residuals when the build keeps a checkpoint
+constexpr int kBuildCkptPeriod = BPC_BUILD_CKPT_PERIOD;
 
 // ---- workspace layouts -----------------------------------------------------
 // Decode, per slice sl = (b Hkv + h) nslices + s: candidates [kSlice] u32
@@ -102,6 +107,7 @@ struct DecodeLayout {
 struct BuildLayout {
   int nchunks;
   size_t off_part, off_p64, off_g64, total;
+  size_t off_ck, total_ck;  // the residual checkpoint, when the workspace holds one
 };
 
 DecodeLayout decode_layout(int B, int Hq, int Hkv, int N, int L, int k);
@@ -185,7 +191,7 @@ hipError_t launch_hash_mm(const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t
 hipError_t launch_build(const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t sK_n, int B, int Hkv,
                         int N, int L, const float* G, float* P, uint32_t* codes, int64_t sC_b,
                         int64_t sC_h, float* err, unsigned long long* fragile, char* ws,
-                        hipStream_t stream);
+                        bool checkpoint, hipStream_t stream);
 
 // ---- device helpers ----------------------------------------------------------
 __device__ __forceinline__ double bf16_to_f64(uint16_t b) {

@@ -36,9 +36,13 @@ namespace bpc {
 //                       P[i] = (float)v (and its fp64 widening for the next
 //                       passes).
 // A final build_bit pass (bit == L) recomputes the last residual and writes
-// ||R_j||.  Nothing of size N x D is stored: the pass reads the keys again,
-// trading fp64 arithmetic (about L^2 D / 2 fused subtractions per key over the
-// whole build) for memory traffic.
+// ||R_j||.  Without a checkpoint nothing of size N x D is stored: the pass
+// reads the keys again, trading fp64 arithmetic (about L^2 D / 2 fused
+// subtractions per key over the whole build) for memory traffic.  With one,
+// the pass at every multiple m T of kBuildCkptPeriod also stores R after m T
+// bits (1 KiB per key, in place) and the passes up to (m + 1) T start from
+// it: at most T subtractions per pass, for a 1 KiB read instead of the
+// 256-byte key.
 // ============================================================================
 
 // the partner lane's value at lane ^ M (quad permutes for 1 and 2)
@@ -90,7 +94,7 @@ __global__ __launch_bounds__(kBuildThreads) void build_bit_kernel(
     const uint16_t* __restrict__ K, int64_t sK_b, int64_t sK_h, int64_t sK_n, int Hkv, int N, int L, int bit,
     const double* __restrict__ G64, const double* __restrict__ P64, uint32_t* __restrict__ codes, int64_t sC_b,
     int64_t sC_h, double* __restrict__ part, int nchunks, float* __restrict__ err,
-    unsigned long long* __restrict__ fragile) {
+    unsigned long long* __restrict__ fragile, double* __restrict__ ck, int ck_from, int ck_store) {
   __shared__ double xch[kBuildGroups][4][64];         // per-block partial dots of each key
   __shared__ double groot[kBuildGroups][kHeadDim];    // tree root of each key group
   __shared__ int frag;
@@ -109,15 +113,31 @@ __global__ __launch_bounds__(kBuildThreads) void build_bit_kernel(
 #pragma unroll
   for (int w = 0; w < W; ++w) cw[w] = 0u;
   uint32_t* crow = codes + b * sC_b + h * sC_h + (int64_t)(valid ? key : 0) * W;
+  // this lane's 32 coordinates in the checkpoint: element e of the block at
+  // ckrow[(e / 2) * 64 + lane], so that each load covers 1 KiB of the
+  // wavefront's keys
+  typedef double f64x2 __attribute__((ext_vector_type(2)));
+  f64x2* ckrow = ck ? reinterpret_cast<f64x2*>(ck + ((((size_t)bh * nchunks + blockIdx.x) * kBuildGroups + grp) * 4 +
+                                                     c) * (32 * 64)) + lane
+                    : nullptr;
   if (valid) {
-    const uint16_t* krow = K + b * sK_b + h * sK_h + (int64_t)key * sK_n + 32 * c;
+    if (ck_from > 0) {
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const uint4 v = *reinterpret_cast<const uint4*>(krow + 8 * q);
-      const uint32_t wd[4] = {v.x, v.y, v.z, v.w};
+      for (int e2 = 0; e2 < 16; ++e2) {
+        const f64x2 x = __builtin_nontemporal_load(ckrow + 64 * e2);
+        r[2 * e2] = x.x;
+        r[2 * e2 + 1] = x.y;
+      }
+    } else {
+      const uint16_t* krow = K + b * sK_b + h * sK_h + (int64_t)key * sK_n + 32 * c;
 #pragma unroll
-      for (int e = 0; e < 8; ++e)
-        r[8 * q + e] = bf16_to_f64((uint16_t)((e & 1) ? (wd[e >> 1] >> 16) : (wd[e >> 1] & 0xFFFFu)));
+      for (int q = 0; q < 4; ++q) {
+        const uint4 v = *reinterpret_cast<const uint4*>(krow + 8 * q);
+        const uint32_t wd[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          r[8 * q + e] = bf16_to_f64((uint16_t)((e & 1) ? (wd[e >> 1] >> 16) : (wd[e >> 1] & 0xFFFFu)));
+      }
     }
 #pragma unroll
     for (int w = 0; w < W; ++w)
@@ -126,17 +146,26 @@ __global__ __launch_bounds__(kBuildThreads) void build_bit_kernel(
 #pragma unroll
     for (int e = 0; e < 32; ++e) r[e] = 0.0;  // never contributes: padded below
   }
-  // the residual after bits 0 .. bit - 1
+  // the residual after bits 0 .. bit - 1: bits ck_from .. bit - 1 removed
+  // from the checkpoint (or all of them from the key)
   const_ptr<double> prow = uniform_ptr(P64 + (size_t)bh * L * kHeadDim + 32 * c);
 #pragma unroll
   for (int w = 0; w < W; ++w) {
+    const int ib0 = max(0, ck_from - 32 * w);
     const int nb = min(32, bit - 32 * w);
     const uint32_t word = cw[w];
-    for (int ib = 0; ib < nb; ++ib) {
+    for (int ib = ib0; ib < nb; ++ib) {
       const double sg = ((word >> ib) & 1u) ? -1.0 : 1.0;
       const_ptr<double> p = prow + (size_t)(32 * w + ib) * kHeadDim;
 #pragma unroll
       for (int e = 0; e < 32; ++e) r[e] = __builtin_fma(sg, p[e], r[e]);
+    }
+  }
+  if (ck_store && valid) {
+#pragma unroll
+    for (int e2 = 0; e2 < 16; ++e2) {
+      const f64x2 x = {r[2 * e2], r[2 * e2 + 1]};
+      __builtin_nontemporal_store(x, ckrow + 64 * e2);
     }
   }
   if (final_pass) {
@@ -260,11 +289,20 @@ template <int W>
 static void launch_build_W(const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t sK_n, int B, int Hkv, int N,
                            int L, const double* G64, float* P, double* P64, uint32_t* codes, int64_t sC_b,
                            int64_t sC_h, float* err, unsigned long long* fragile, double* part, int nchunks,
-                           hipStream_t stream) {
+                           double* ck, hipStream_t stream) {
   const dim3 grid(nchunks, B * Hkv);
   for (int bit = 0; bit <= L; ++bit) {
+    // With a checkpoint buffer the pass at bit m T stores R after m T bits,
+    // and the passes up to the next one start from it.
+    int from = 0, store = 0;
+    if (ck) {
+      from = bit - (bit % kBuildCkptPeriod == 0 ? kBuildCkptPeriod : bit % kBuildCkptPeriod);
+      from = max(from, 0);
+      store = (bit > 0 && bit < L && bit % kBuildCkptPeriod == 0) ? 1 : 0;
+    }
     build_bit_kernel<W><<<grid, kBuildThreads, 0, stream>>>(K, sK_b, sK_h, sK_n, Hkv, N, L, bit, G64, P64, codes,
-                                                           sC_b, sC_h, part, nchunks, err, fragile);
+                                                           sC_b, sC_h, part, nchunks, err, fragile, ck, from,
+                                                           store);
     if (bit == L) break;
     build_finish_kernel<<<B * Hkv, kFinishBlocks * kHeadDim, 0, stream>>>(N, L, bit, nchunks, part, P, P64);
   }
@@ -272,9 +310,10 @@ static void launch_build_W(const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_
 
 hipError_t launch_build(const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t sK_n, int B, int Hkv, int N,
                         int L, const float* G, float* P, uint32_t* codes, int64_t sC_b, int64_t sC_h,
-                        float* err, unsigned long long* fragile, char* ws, hipStream_t stream) {
+                        float* err, unsigned long long* fragile, char* ws, bool checkpoint, hipStream_t stream) {
   const BuildLayout lay = build_layout(B, Hkv, N, L);
   double* part = reinterpret_cast<double*>(ws + lay.off_part);
+  double* ck = checkpoint ? reinterpret_cast<double*>(ws + lay.off_ck) : nullptr;
   double* P64 = reinterpret_cast<double*>(ws + lay.off_p64);
   double* G64 = reinterpret_cast<double*>(ws + lay.off_g64);
   const int ng = L * kHeadDim;
@@ -282,15 +321,15 @@ hipError_t launch_build(const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t s
   switch (L) {
     case 32:
       launch_build_W<1>(K, sK_b, sK_h, sK_n, B, Hkv, N, L, G64, P, P64, codes, sC_b, sC_h, err, fragile, part,
-                        lay.nchunks, stream);
+                        lay.nchunks, ck, stream);
       break;
     case 64:
       launch_build_W<2>(K, sK_b, sK_h, sK_n, B, Hkv, N, L, G64, P, P64, codes, sC_b, sC_h, err, fragile, part,
-                        lay.nchunks, stream);
+                        lay.nchunks, ck, stream);
       break;
     default:
       launch_build_W<4>(K, sK_b, sK_h, sK_n, B, Hkv, N, L, G64, P, P64, codes, sC_b, sC_h, err, fragile, part,
-                        lay.nchunks, stream);
+                        lay.nchunks, ck, stream);
       break;
   }
   return hipGetLastError();

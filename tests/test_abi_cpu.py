@@ -66,6 +66,11 @@ def test_workspace_sizes(lib):
     # widened to fp64; no N x D residual
     assert b >= 2 * 8 * ((1000 + 127) // 128) * 128 * 8 + 2 * 8 * 64 * 128 * 8 + 64 * 128 * 8
     assert b < 2 * 8 * 1000 * 128 * 8 // 4
+    # with the residual checkpoint: 1 KiB more per key, padded to 128-key chunks
+    lib.bpc_build_checkpoint_workspace_bytes.restype = ctypes.c_size_t
+    bc = lib.bpc_build_checkpoint_workspace_bytes(2, 8, 1000, 128, 64)
+    assert bc - b >= 2 * 8 * 1024 * 128 * 8 and (bc - b) % 256 == 0 and bc < b + 2 * 8 * 1024 * 128 * 8 + 256
+    assert lib.bpc_build_checkpoint_workspace_bytes(2, 8, 1000, 64, 64) == 0  # D != 128
 
 
 _i64 = ctypes.c_int64

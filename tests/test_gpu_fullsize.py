@@ -129,9 +129,11 @@ def layer_with_recorded_heads(cfg, layer, recs):
 
 
 def build_layer(cfg, d):
+    # the whole layer with the residual checkpoint; check_build rebuilds one
+    # head without it
     err = torch.empty(cfg.B, cfg.Hkv, cfg.N, device=DEV)
     frag = torch.zeros(1, dtype=torch.int64, device=DEV)
-    P, codes, _ = bpc.build_hash(d["K"], d["G"], err_out=err, fragile=frag)
+    P, codes, _ = bpc.build_hash(d["K"], d["G"], err_out=err, fragile=frag, checkpoint=True)
     return P, codes, err, frag
 
 

@@ -91,9 +91,10 @@ def test_build_parity_tiny(tiny):
     assert int(frag.item()) == nfrag
 
 
+@pytest.mark.parametrize("checkpoint", [False, True], ids=["recompute", "checkpoint"])
 @pytest.mark.parametrize("L,N,B,H", [(64, 1000, 2, 2), (128, 300, 1, 3), (32, 513, 1, 1)])
-def test_build_parity_ragged_strided(L, N, B, H):
-    announce(f"[build ragged] L={L} N={N} B={B} H={H}")
+def test_build_parity_ragged_strided(L, N, B, H, checkpoint):
+    announce(f"[build ragged] L={L} N={N} B={B} H={H} checkpoint={checkpoint}")
     rng = np.random.default_rng(L + N)
     Ncap = N + 24
     A = rng.standard_normal((8, 128))
@@ -101,7 +102,7 @@ def test_build_parity_ragged_strided(L, N, B, H):
     K = torch.from_numpy(Kf.astype(np.float32)).to(torch.bfloat16).to(DEV)
     G = torch.from_numpy(rng.standard_normal((L, 128)).astype(np.float32)).to(DEV)
     codes = torch.zeros(B, H, Ncap, L // 32, dtype=torch.int32, device=DEV)
-    P, codes, _ = bpc.build_hash(K, G, N=N, codes_out=codes)
+    P, codes, _ = bpc.build_hash(K, G, N=N, codes_out=codes, checkpoint=checkpoint)
     torch.cuda.synchronize()
     Kb = bits(K)
     for b in range(B):
