@@ -57,6 +57,9 @@ def parse():
     ap.add_argument("--summarize", metavar="DIR", nargs="+", default=None,
                     help="summarize rocprofv3 csv output under each DIR (kernel stats and counters per dispatch) "
                          "instead of benchmarking")
+    ap.add_argument("--prefill-only", metavar="WORKLOAD", default=None,
+                    help="time only the prefill of one layer of WORKLOAD: Algorithm 1 recomputing its residual, "
+                         "then with the residual checkpoint, then Algorithm 2 on both kernels; print one JSON line")
     ap.add_argument("--pmc-json", metavar="PATH", default=None,
                     help="with --summarize over a FETCH_SIZE and a WRITE_SIZE run: write HBM bytes per launch")
     return ap.parse_args()
@@ -77,6 +80,38 @@ def source_sha() -> str:
             if line:
                 h.update(line.encode() + b"\n")
     return h.hexdigest()[:16]
+
+
+def _build_passes(path, root):
+    """The Algorithm 1 builds of a kernel trace, one line each: the passes
+    (build_bit launches, one per bit and a last one for the errors) and the
+    time of the bit passes by range of bits."""
+    import csv
+    rows = []
+    for r in csv.DictReader(open(path)):
+        n = r["Kernel_Name"]
+        if "bpc::build_" in n:
+            rows.append((int(r["Start_Timestamp"]), int(r["End_Timestamp"]), _short(n)))
+    rows.sort()
+    builds, cur = [], None
+    for t0, t1, n in rows:
+        if "build_prep" in n:
+            cur = {"bit": [], "finish": [], "t0": t0, "t1": t1}
+            builds.append(cur)
+        elif cur is not None:
+            cur["bit" if "build_bit" in n else "finish"].append((t1 - t0) / 1e3)
+            cur["t1"] = t1
+    out = []
+    if builds:
+        out.append(f"Algorithm 1 builds ({os.path.relpath(path, root)}), durations in us:")
+    for i, b in enumerate(builds):
+        bit = b["bit"]
+        nb = len(bit)
+        rng = [(a, min(e, nb - 1)) for a, e in ((0, 16), (16, 32), (32, 64), (64, nb - 1))] + [(nb - 1, nb)]
+        parts = ", ".join(f"passes {a}-{e - 1}: mean {sum(bit[a:e]) / (e - a):.1f}" for a, e in rng if e > a)
+        out.append(f"  build {i}: {len(bit)} bit passes, {sum(bit) / 1e3:.2f} ms in them, {sum(b['finish']) / 1e3:.2f} ms "
+                   f"in {len(b['finish'])} fold and finish launches, {(b['t1'] - b['t0']) / 1e6:.2f} ms first to last; {parts}")
+    return out
 
 
 def _short(name: str) -> str:
@@ -119,6 +154,8 @@ def summarize(roots, pmc_json=None) -> None:
                     lines.append(f"{_short(r['Name'])[:47]:<48}{int(r['Calls']):>8}"
                                  f"{float(r['AverageNs']) / 1e3:>12.2f}{float(r.get('MinNs', 'nan')) / 1e3:>10.2f}"
                                  f"{float(r.get('MaxNs', 'nan')) / 1e3:>10.2f}{float(r['TotalDurationNs']) / 1e6:>12.3f}")
+        for f in sorted(glob.glob(os.path.join(root, "**", "*kernel_trace.csv"), recursive=True)):
+            lines.extend(_build_passes(f, root))
         for f in sorted(glob.glob(os.path.join(root, "**", "*counter_collection.csv"), recursive=True)):
             acc = defaultdict(lambda: defaultdict(list))
             copies = defaultdict(list)
@@ -310,6 +347,44 @@ def copy_ceiling(dev):
             "what": "torch copy of 1 GiB (1 GiB read + 1 GiB written), mean of 10"}
 
 
+def prefill_only(name):
+    """Prefill of one layer of a workload, each kernel path once after a
+    warm-up build: Algorithm 1 recomputing the residual, Algorithm 1 with
+    the residual checkpoint (results compared), Algorithm 2 fp64 and on the
+    matrix cores (codes compared)."""
+    import torch
+
+    import paper_2608_04405_amd as bpc
+    from workloads import config_by_name, make_layer
+    cfg = config_by_name(name)
+    dev = torch.device("cuda:0")
+    B, Hkv, N, L = cfg.B, cfg.Hkv, cfg.N, cfg.L
+    d = make_layer(cfg, layer=0, device=dev)
+    K, G = d["K"], d["G"].to(dev)
+    del d
+    ws = torch.empty(bpc.build_checkpoint_workspace_bytes(B, Hkv, N, L), dtype=torch.uint8, device=dev)
+    small = ws[:bpc.build_workspace_bytes(B, Hkv, N, L)]
+    bpc.build_hash(K, G, workspace=small)  # warm-up
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
+    ev[0].record()
+    P1, c1, _ = bpc.build_hash(K, G, workspace=small)
+    ev[1].record()
+    P2, c2, _ = bpc.build_hash(K, G, workspace=ws)
+    ev[2].record()
+    h1, _ = bpc.hash_keys(K, P1)
+    ev[3].record()
+    h2 = bpc.hash_keys_mm(K, P1)
+    ev[4].record()
+    torch.cuda.synchronize()
+    if not (torch.equal(P1, P2) and torch.equal(c1, c2) and torch.equal(h1, h2)):
+        raise RuntimeError(f"{name}: the prefill paths disagree")
+    t = [ev[i].elapsed_time(ev[i + 1]) for i in range(4)]
+    print(json.dumps({"workload": name, "keys": B * Hkv * N, "L": L, "build_ms": round(t[0], 3),
+                      "build_checkpoint_ms": round(t[1], 3), "hash_ms": round(t[2], 3), "hash_mm_ms": round(t[3], 3),
+                      "checkpoint_workspace_bytes": int(ws.numel())}), flush=True)
+
+
 def main():
     args = parse()
     if args.summarize:
@@ -319,6 +394,9 @@ def main():
         print("bench.py measures one GPU: this build has no multi-GPU path (the decode step of every "
               "(sequence, KV head) is independent; see DESIGN.md for how it would shard).", file=sys.stderr)
         sys.exit(2)
+    if args.prefill_only:
+        prefill_only(args.prefill_only)
+        return
 
     import torch
 

@@ -116,6 +116,9 @@ BuildLayout build_layout(int B, int Hkv, int N, int L) {
   size_t o = 0;
   b.off_part = o;  // one fp64 tree sum per chunk and coordinate
   o = align_up(o + BH * b.nchunks * (size_t)kHeadDim * sizeof(double), 256);
+  b.nfold = b.nchunks > 8 * kBuildFold ? (b.nchunks + kBuildFold - 1) / kBuildFold : 0;
+  b.off_fold = o;  // one fp64 tree sum per block of chunks and coordinate
+  o = align_up(o + BH * b.nfold * (size_t)kHeadDim * sizeof(double), 256);
   b.off_p64 = o;   // P widened to fp64, the scalar operand of the residual
   o = align_up(o + BH * (size_t)L * kHeadDim * sizeof(double), 256);
   b.off_g64 = o;   // G widened to fp64

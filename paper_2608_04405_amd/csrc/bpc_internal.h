@@ -78,6 +78,9 @@ constexpr int kBuildChunk = 64 * kBuildGroups;     // keys per workgroup (one ch
 #endif
 // bits between stored fp64 residuals when the build keeps a checkpoint
 constexpr int kBuildCkptPeriod = BPC_BUILD_CKPT_PERIOD;
+// chunk sums folded per workgroup before the per-(b, h) reduction, when a
+// (b, h) has more than 8 such blocks of chunks
+constexpr int kBuildFold = 32;
 
 // ---- workspace layouts -----------------------------------------------------
 // Decode, per slice sl = (b Hkv + h) nslices + s: candidates [kSlice] u32
@@ -106,7 +109,8 @@ struct DecodeLayout {
 
 struct BuildLayout {
   int nchunks;
-  size_t off_part, off_p64, off_g64, total;
+  int nfold;  // aligned blocks of kBuildFold chunks folded first, or 0
+  size_t off_part, off_fold, off_p64, off_g64, total;
   size_t off_ck, total_ck;  // the residual checkpoint, when the workspace holds one
 };
 

@@ -32,7 +32,10 @@ namespace bpc {
 //                       rows, +0 past N, formed across lanes by a reduce-scatter
 //                       butterfly (each level halves the coordinates a lane
 //                       carries) and across the key groups in LDS.
-//   build_finish_kernel pairwise tree over the chunk sums, v = s / N,
+//   build_fold_kernel   (more than 8 x 32 chunks per (b, h)) the subtrees over
+//                       aligned blocks of 32 chunk sums, many workgroups
+//   build_finish_kernel pairwise tree over the chunk sums (or those subtrees),
+//                       v = s / N,
 //                       P[i] = (float)v (and its fp64 widening for the next
 //                       passes).
 // A final build_bit pass (bit == L) recomputes the last residual and writes
@@ -221,6 +224,28 @@ __global__ __launch_bounds__(kBuildThreads) void build_bit_kernel(
   if (fragile && threadIdx.x == 0 && frag) atomicAdd(fragile, (unsigned long long)frag);
 }
 
+// Thread d of workgroup (x, bh) folds the aligned block of chunk sums
+// [x kBuildFold, (x + 1) kBuildFold) of coordinate d, level by level with the
+// odd one carried (the last block may be short): the subtree of the pairwise
+// tree over those chunks.
+__global__ __launch_bounds__(kHeadDim) void build_fold_kernel(const double* __restrict__ part, int nchunks,
+                                                              double* __restrict__ fold, int nfold) {
+  const int bh = blockIdx.y, x = blockIdx.x, d = threadIdx.x;
+  const int begin = x * kBuildFold;
+  int c = min(kBuildFold, nchunks - begin);
+  const double* src = part + ((size_t)bh * nchunks + begin) * kHeadDim + d;
+  double v[kBuildFold];
+#pragma unroll
+  for (int e = 0; e < kBuildFold; ++e) v[e] = (e < c) ? src[(size_t)e * kHeadDim] : 0.0;
+#pragma unroll
+  for (int w = kBuildFold / 2; w >= 1; w >>= 1) {
+#pragma unroll
+    for (int i = 0; i < w; ++i) v[i] = (2 * i + 1 < c) ? dadd(v[2 * i], v[2 * i + 1]) : v[2 * i];
+    c = (c + 1) >> 1;
+  }
+  fold[((size_t)bh * nfold + x) * kHeadDim + d] = v[0];
+}
+
 // One workgroup per (b, h): thread (blk, d) folds an aligned block of S
 // chunk sums of coordinate d (S a power of two, 8 blocks cover all chunks) as
 // a binary counter, and the block roots are then paired level by level in LDS
@@ -289,7 +314,7 @@ template <int W>
 static void launch_build_W(const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t sK_n, int B, int Hkv, int N,
                            int L, const double* G64, float* P, double* P64, uint32_t* codes, int64_t sC_b,
                            int64_t sC_h, float* err, unsigned long long* fragile, double* part, int nchunks,
-                           double* ck, hipStream_t stream) {
+                           double* fold, int nfold, double* ck, hipStream_t stream) {
   const dim3 grid(nchunks, B * Hkv);
   for (int bit = 0; bit <= L; ++bit) {
     // With a checkpoint buffer the pass at bit m T stores R after m T bits,
@@ -304,7 +329,12 @@ static void launch_build_W(const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_
                                                            sC_b, sC_h, part, nchunks, err, fragile, ck, from,
                                                            store);
     if (bit == L) break;
-    build_finish_kernel<<<B * Hkv, kFinishBlocks * kHeadDim, 0, stream>>>(N, L, bit, nchunks, part, P, P64);
+    if (nfold) {
+      build_fold_kernel<<<dim3(nfold, B * Hkv), kHeadDim, 0, stream>>>(part, nchunks, fold, nfold);
+      build_finish_kernel<<<B * Hkv, kFinishBlocks * kHeadDim, 0, stream>>>(N, L, bit, nfold, fold, P, P64);
+    } else {
+      build_finish_kernel<<<B * Hkv, kFinishBlocks * kHeadDim, 0, stream>>>(N, L, bit, nchunks, part, P, P64);
+    }
   }
 }
 
@@ -314,6 +344,7 @@ hipError_t launch_build(const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t s
   const BuildLayout lay = build_layout(B, Hkv, N, L);
   double* part = reinterpret_cast<double*>(ws + lay.off_part);
   double* ck = checkpoint ? reinterpret_cast<double*>(ws + lay.off_ck) : nullptr;
+  double* fold = reinterpret_cast<double*>(ws + lay.off_fold);
   double* P64 = reinterpret_cast<double*>(ws + lay.off_p64);
   double* G64 = reinterpret_cast<double*>(ws + lay.off_g64);
   const int ng = L * kHeadDim;
@@ -321,15 +352,15 @@ hipError_t launch_build(const uint16_t* K, int64_t sK_b, int64_t sK_h, int64_t s
   switch (L) {
     case 32:
       launch_build_W<1>(K, sK_b, sK_h, sK_n, B, Hkv, N, L, G64, P, P64, codes, sC_b, sC_h, err, fragile, part,
-                        lay.nchunks, ck, stream);
+                        lay.nchunks, fold, lay.nfold, ck, stream);
       break;
     case 64:
       launch_build_W<2>(K, sK_b, sK_h, sK_n, B, Hkv, N, L, G64, P, P64, codes, sC_b, sC_h, err, fragile, part,
-                        lay.nchunks, ck, stream);
+                        lay.nchunks, fold, lay.nfold, ck, stream);
       break;
     default:
       launch_build_W<4>(K, sK_b, sK_h, sK_n, B, Hkv, N, L, G64, P, P64, codes, sC_b, sC_h, err, fragile, part,
-                        lay.nchunks, ck, stream);
+                        lay.nchunks, fold, lay.nfold, ck, stream);
       break;
   }
   return hipGetLastError();
