@@ -46,7 +46,10 @@ namespace bpc {
 typedef short bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
-constexpr int kHmThreads = 256;      // four wavefronts, 64 keys per wavefront per iteration
+// 64 keys per wavefront per iteration; four wavefronts per workgroup, eight
+// at L = 128, where one workgroup fills a CU's LDS
+template <int L>
+constexpr int hm_threads() { return L == 128 ? 512 : 256; }
 constexpr int kHmPsStride = 132;     // fp32 P row stride in LDS (floats)
 constexpr int kHmXsStride = 20;      // transpose buffer row stride (floats)
 
@@ -130,17 +133,28 @@ __device__ __forceinline__ double hm_reference_decision(const uint16_t* krow, co
   return dadd(dadd(s0, s1), dadd(s2, s3));
 }
 
+// The Gram matrix by rows, each row t holding the 16-wide column blocks from
+// t's own block on: G[t][i] (t < i) at hm_gram_row<L>(t) + i - 16 (t / 16).
+template <int L>
+__device__ __forceinline__ int hm_gram_row(int t) {
+  constexpr int nb = L / 16;
+  const int a = t >> 4, r = t & 15;
+  return 16 * (16 * (nb * a - a * (a - 1) / 2) + r * (nb - a));
+}
+template <int L>
+constexpr int hm_gram_size() { return 256 * (L / 16) * (L / 16 + 1) / 2; }
+
 template <int L>
 struct HmShared {
   float Ps[L * kHmPsStride];              // P of this (b, h), fp32
-  float Gs[L * L];                        // Gs[t L + i] = fp32(P_t . P_i) for t < i
+  float Gs[hm_gram_size<L>()];            // fp32(P_t . P_i) for t < i, rows as hm_gram_row
   float4 cst[L];                          // per bit: |P_i|, c1, c2, c3 (see hm_bound)
-  float Xs[4][64 * kHmXsStride];          // per wavefront: MFMA tile -> one key per lane (also setup scratch)
+  float Xs[hm_threads<L>() / 64][64 * kHmXsStride];  // per wavefront: MFMA tile -> one key per lane (also setup scratch)
   unsigned int nfrag, nfall;
 };
 
 template <int L>
-__global__ __launch_bounds__(kHmThreads, L <= 64 ? 2 : 1) void hash_mm_kernel(const uint16_t* __restrict__ K, int64_t sK_b,
+__global__ __launch_bounds__(hm_threads<L>(), 2) void hash_mm_kernel(const uint16_t* __restrict__ K, int64_t sK_b,
                                                              int64_t sK_h, int64_t sK_n, int Hkv, int N,
                                                              const float* __restrict__ P, int64_t sP_b, int64_t sP_h,
                                                              uint32_t* __restrict__ codes, int64_t sC_b,
@@ -148,6 +162,8 @@ __global__ __launch_bounds__(kHmThreads, L <= 64 ? 2 : 1) void hash_mm_kernel(co
                                                              unsigned long long* __restrict__ fallbacks,
                                                              int keys_per_wg) {
   constexpr int W = L / 32;
+  constexpr int kHmThreads = hm_threads<L>();
+  constexpr int NWV = kHmThreads / 64;
   __shared__ __align__(16) HmShared<L> sh;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int bh = blockIdx.y;
@@ -176,7 +192,7 @@ __global__ __launch_bounds__(kHmThreads, L <= 64 ? 2 : 1) void hash_mm_kernel(co
         s = fma((double)x.z, (double)y.z, s);
         s = fma((double)x.w, (double)y.w, s);
       }
-      sh.Gs[t * L + i] = (float)s;
+      sh.Gs[hm_gram_row<L>(t) + i - 16 * (t >> 4)] = (float)s;
     }
   }
   if (tid < kHeadDim) {
@@ -193,7 +209,8 @@ __global__ __launch_bounds__(kHmThreads, L <= 64 ? 2 : 1) void hash_mm_kernel(co
   if (tid < L) {
     const int i = tid;
     double cabs = 0.0, q = 0.0;
-    for (int t = 0; t < i; ++t) cabs += fabs((double)sh.Gs[t * L + i]) + 0x1p-20 * nP[t] * nP[i];
+    for (int t = 0; t < i; ++t)
+      cabs += fabs((double)sh.Gs[hm_gram_row<L>(t) + i - 16 * (t >> 4)]) + 0x1p-20 * nP[t] * nP[i];
     for (int d = 0; d < kHeadDim; ++d) q += Ad[d] * fabs((double)sh.Ps[i * kHmPsStride + d]);
     const double up = 1.0 + 0x1p-20;
     const double c1 = (136.0 * 0x1p-24 + (36.0 + i) * 0x1p-53) * up;
@@ -210,7 +227,7 @@ __global__ __launch_bounds__(kHmThreads, L <= 64 ? 2 : 1) void hash_mm_kernel(co
   const int key_begin = blockIdx.x * keys_per_wg;
   const int key_end = min(N, key_begin + keys_per_wg);
   unsigned int nfrag = 0, nfall = 0;
-  for (int base = key_begin + wave * 64; base < key_end; base += 4 * 64) {
+  for (int base = key_begin + wave * 64; base < key_end; base += NWV * 64) {
     // B operands: lane i holds key base + 16 tau + i % 16, coordinates
     // 32 m + 8 (i / 16) .. + 7
     uint4 kv[4][4];
@@ -284,7 +301,8 @@ __global__ __launch_bounds__(kHmThreads, L <= 64 ? 2 : 1) void hash_mm_kernel(co
 #pragma unroll 4
         for (int tt = 0; tt < nb; ++tt) {
           const float sg = ((word >> tt) & 1u) ? -1.f : 1.f;
-          const float4* gr = reinterpret_cast<const float4*>(&sh.Gs[(32 * w + tt) * L + 16 * T]);
+          const int t = 32 * w + tt;
+          const float4* gr = reinterpret_cast<const float4*>(&sh.Gs[hm_gram_row<L>(t) + 16 * T - 16 * (t >> 4)]);
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
             const float4 g = gr[q];
@@ -321,7 +339,7 @@ __global__ __launch_bounds__(kHmThreads, L <= 64 ? 2 : 1) void hash_mm_kernel(co
           ub |= (u ? 1u : 0u) << i;
           if (i < 15) {
             const float sg = u ? -1.f : 1.f;
-            const float4* gr = reinterpret_cast<const float4*>(&sh.Gs[bit * L + 16 * T]);
+            const float4* gr = reinterpret_cast<const float4*>(&sh.Gs[hm_gram_row<L>(bit)]);
 #pragma unroll
             for (int q = (i + 1) / 4; q < 4; ++q) {
               const float4 g = gr[q];
@@ -398,6 +416,7 @@ static hipError_t launch_hash_mm_L(const uint16_t* K, int64_t sK_b, int64_t sK_h
                                    int64_t sC_h, unsigned long long* fragile, unsigned long long* fallbacks,
                                    hipStream_t stream) {
   static_assert(sizeof(HmShared<L>) <= 160 * 1024, "LDS budget");
+  constexpr int kHmThreads = hm_threads<L>();
   // about 2048 workgroups in all, each over whole wavefront iterations
   const long long total = (long long)B * Hkv * N;
   long long per = (total + 2047) / 2048;
