@@ -13,7 +13,10 @@
 // cut into three bf16 parts (hi + mid + lo, by truncation, exactly P), and
 // the products accumulate in fp32.  The corrections run in fp32 on the
 // vector units with the Gram matrix (fp64, rounded to fp32) as wavefront-
-// uniform operands.
+// uniform operands; at L = 128 the corrections by earlier 16-bit blocks are
+// one more bf16 contraction (signs +-1 times the Gram entries cut like P,
+// the hi products in a chain of their own) and only each block's own
+// triangle stays on the vector units.
 //
 // The fp32 value a^ differs from the value a the fixed-order fp64 reference
 // computes (canonical residual, four-block dot) by at most
@@ -30,7 +33,11 @@
 // corrections and the Gram matrix's rounding to fp32, the third the
 // reference's own rounding (i rounded subtractions per coordinate and the
 // 34 roundings of a four-block dot), the last two underflow of bf16 parts
-// and products.  The evaluation of E_i in fp32 is covered by a factor
+// and products.  With the corrections on the matrix cores the bound takes
+// 138 u S, (i + 4) in place of (i + 2) before 2.01 C_i, and 2^-109: the
+// mid/lo chain gains at most 32 roundings per earlier block of sums below
+// 2^-7 (S + C_i), the hi chain at most 16 T roundings of sums below C_i, and
+// one addition joins it.  The evaluation of E_i in fp32 is covered by a factor
 // 1 + 2^-8.  When |a^| > E_i + 1.01e-6 the reference's sign is that of a^,
 // and |fp32(a)| >= 1e-6, so the decision is not fragile.  Otherwise (a few
 // keys in ten thousand, and every decision near zero), the wavefront
@@ -144,10 +151,50 @@ __device__ __forceinline__ int hm_gram_row(int t) {
 template <int L>
 constexpr int hm_gram_size() { return 256 * (L / 16) * (L / 16 + 1) / 2; }
 
+// At L = 128 the corrections by earlier blocks run on the matrix cores (see
+// the main loop), and the Gram matrix (the same 36 KB) is kept as the 16 x 16
+// diagonal blocks (row t, column i % 16 at 256 (t / 16) + 16 (t % 16) +
+// i % 16), then, for every bit i of block T >= 1, the 16 T entries G[t][i],
+// t < 16 T, contiguous (the matrix-core operand reads 8 consecutive t).
+template <int L>
+constexpr bool hm_mm_corr() { return L == 128; }
+template <int L>
+__device__ __forceinline__ int hm_gram_col(int i) {  // the entries G[t][i], t < 16 (i / 16)
+  constexpr int nb = L / 16;
+  const int T = i >> 4;
+  return 256 * nb + 256 * (T * (T - 1) / 2) + 16 * T * (i & 15);
+}
+// the index of G[t][i], t < i
+template <int L>
+__device__ __forceinline__ int hm_gram_at(int t, int i) {
+  if constexpr (hm_mm_corr<L>()) {
+    if ((t >> 4) == (i >> 4)) return 256 * (t >> 4) + 16 * (t & 15) + (i & 15);
+    return hm_gram_col<L>(i) + t;
+  } else {
+    return hm_gram_row<L>(t) + i - 16 * (t >> 4);
+  }
+}
+// G[t][16 (t / 16) .. + 15], the row of t inside its own column block
+template <int L>
+__device__ __forceinline__ int hm_gram_diag(int t) {
+  if constexpr (hm_mm_corr<L>()) return 256 * (t >> 4) + 16 * (t & 15);
+  else return hm_gram_row<L>(t);
+}
+
+// Eight bf16 operands +-1 from the bits of `byte` (bit set: -1), low half of
+// each word first; all zero when !on
+__device__ __forceinline__ uint4 sign_operand(uint32_t byte, bool on) {
+  uint32_t w[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k)
+    w[k] = on ? (0x3F803F80u | (((byte >> (2 * k)) & 1u) << 15) | (((byte >> (2 * k + 1)) & 1u) << 31)) : 0u;
+  return make_uint4(w[0], w[1], w[2], w[3]);
+}
+
 template <int L>
 struct HmShared {
   float Ps[L * kHmPsStride];              // P of this (b, h), fp32
-  float Gs[hm_gram_size<L>()];            // fp32(P_t . P_i) for t < i, rows as hm_gram_row
+  float Gs[hm_gram_size<L>()];            // fp32(P_t . P_i) for t < i, at hm_gram_at(t, i)
   float4 cst[L];                          // per bit: |P_i|, c1, c2, c3 (see hm_bound)
   float Xs[hm_threads<L>() / 64][64 * kHmXsStride];  // per wavefront: MFMA tile -> one key per lane (also setup scratch)
   unsigned int nfrag, nfall;
@@ -192,7 +239,7 @@ __global__ __launch_bounds__(hm_threads<L>(), 2) void hash_mm_kernel(const uint1
         s = fma((double)x.z, (double)y.z, s);
         s = fma((double)x.w, (double)y.w, s);
       }
-      sh.Gs[hm_gram_row<L>(t) + i - 16 * (t >> 4)] = (float)s;
+      sh.Gs[hm_gram_at<L>(t, i)] = (float)s;
     }
   }
   if (tid < kHeadDim) {
@@ -210,12 +257,17 @@ __global__ __launch_bounds__(hm_threads<L>(), 2) void hash_mm_kernel(const uint1
     const int i = tid;
     double cabs = 0.0, q = 0.0;
     for (int t = 0; t < i; ++t)
-      cabs += fabs((double)sh.Gs[hm_gram_row<L>(t) + i - 16 * (t >> 4)]) + 0x1p-20 * nP[t] * nP[i];
+      cabs += fabs((double)sh.Gs[hm_gram_at<L>(t, i)]) + 0x1p-20 * nP[t] * nP[i];
     for (int d = 0; d < kHeadDim; ++d) q += Ad[d] * fabs((double)sh.Ps[i * kHmPsStride + d]);
     const double up = 1.0 + 0x1p-20;
-    const double c1 = (136.0 * 0x1p-24 + (36.0 + i) * 0x1p-53) * up;
+    // with the corrections on the matrix cores: two more roundings of
+    // 2^-7-sized sums per earlier bit in the mid/lo chain (+2 u S, +2 u C_i)
+    constexpr bool mm = hm_mm_corr<L>();
+    const double c1 = ((mm ? 138.0 : 136.0) * 0x1p-24 + (36.0 + i) * 0x1p-53) * up;
     const double c2 = (i + 2.0) * 0x1p-24;
-    const double c3 = ((i + 2.0) * 0x1p-24 * 2.01 * cabs + q * (36.0 + i) * 0x1p-53 + 0x1p-110 + 1.01e-6) * up;
+    const double c3 = ((i + (mm ? 4.0 : 2.0)) * 0x1p-24 * 2.01 * cabs + q * (36.0 + i) * 0x1p-53 +
+                       (mm ? 0x1p-109 : 0x1p-110) + 1.01e-6) *
+                      up;
     sh.cst[i] = make_float4((float)(nP[i] * up) * (float)up, (float)c1, (float)c2, (float)c3);
   }
   __syncthreads();
@@ -264,9 +316,9 @@ __global__ __launch_bounds__(hm_threads<L>(), 2) void hash_mm_kernel(const uint1
 #pragma unroll
     for (int T = 0; T < L / 16; ++T) {
       // projections of bits 16 T .. 16 T + 15 of the 64 keys
-      f32x4_t ah[4], as[4];
+      f32x4_t ah[4], as[4], ch[4];
 #pragma unroll
-      for (int tau = 0; tau < 4; ++tau) ah[tau] = as[tau] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+      for (int tau = 0; tau < 4; ++tau) ah[tau] = as[tau] = ch[tau] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int m = 0; m < 4; ++m) {
         const float* prow = &sh.Ps[(16 * T + c16) * kHmPsStride + 32 * m + 8 * g4];
@@ -279,11 +331,38 @@ __global__ __launch_bounds__(hm_threads<L>(), 2) void hash_mm_kernel(const uint1
           ah[tau] = mfma32(phi, kv[tau][m], ah[tau]);
         }
       }
+      if constexpr (hm_mm_corr<L>()) {
+        // The corrections by earlier blocks as one more contraction: D[j][key]
+        // = sum_{t < 16 T} fp32(G[t][16 T + j]) s_t(key), s_t = -1 where bit t
+        // of the key is set, else +1 (exact in bf16).  Gram entries are cut
+        // into hi + mid + lo like P; the hi products go to their own chain
+        // ch (sums of size C_i), mid and lo to the small chain as.
+#pragma unroll
+        for (int st = 0; st < (T + 1) / 2; ++st) {
+          const uint32_t cws = cw[st];
+          // lane (g4, c16): A = G[32 st + 8 g4 .. + 7][16 T + c16], B = signs of
+          // the same 8 bits of key 16 tau + c16 (none past 16 T)
+          const bool on = 32 * st + 8 * g4 < 16 * T;
+          uint4 ghi = make_uint4(0u, 0u, 0u, 0u), gmid = ghi, glo = ghi;
+          if (on) {
+            const float* gp = &sh.Gs[hm_gram_col<L>(16 * T + c16) + 32 * st + 8 * g4];
+            split3(*reinterpret_cast<const float4*>(gp), *reinterpret_cast<const float4*>(gp + 4), ghi, gmid, glo);
+          }
+#pragma unroll
+          for (int tau = 0; tau < 4; ++tau) {
+            const uint32_t word = (uint32_t)__shfl((int)cws, 16 * tau + c16, 64);
+            const uint4 sb = sign_operand((word >> (8 * g4)) & 0xFFu, on);
+            ch[tau] = mfma32(ghi, sb, ch[tau]);
+            as[tau] = mfma32(gmid, sb, as[tau]);
+            as[tau] = mfma32(glo, sb, as[tau]);
+          }
+        }
+      }
 #pragma unroll
       for (int tau = 0; tau < 4; ++tau)
         *reinterpret_cast<float4*>(&Xs[(16 * tau + c16) * kHmXsStride + 4 * g4]) =
-            make_float4(ah[tau][0] + as[tau][0], ah[tau][1] + as[tau][1], ah[tau][2] + as[tau][2],
-                        ah[tau][3] + as[tau][3]);
+            make_float4((ah[tau][0] + as[tau][0]) + ch[tau][0], (ah[tau][1] + as[tau][1]) + ch[tau][1],
+                        (ah[tau][2] + as[tau][2]) + ch[tau][2], (ah[tau][3] + as[tau][3]) + ch[tau][3]);
       wave_lds_sync();
       float y[16];
 #pragma unroll
@@ -293,16 +372,17 @@ __global__ __launch_bounds__(hm_threads<L>(), 2) void hash_mm_kernel(const uint1
       }
       wave_lds_sync();
       // corrections by the bits of earlier blocks: y_j -= u_t Gr[t][j]
+      // (on the vector units below L = 128)
 #pragma unroll
       for (int w = 0; w < W; ++w) {
-        if (32 * w >= 16 * T) break;
+        if (hm_mm_corr<L>() || 32 * w >= 16 * T) break;
         const int nb = min(32, 16 * T - 32 * w);
         const uint32_t word = cw[w];
 #pragma unroll 4
         for (int tt = 0; tt < nb; ++tt) {
           const float sg = ((word >> tt) & 1u) ? -1.f : 1.f;
           const int t = 32 * w + tt;
-          const float4* gr = reinterpret_cast<const float4*>(&sh.Gs[hm_gram_row<L>(t) + 16 * T - 16 * (t >> 4)]);
+          const float4* gr = reinterpret_cast<const float4*>(&sh.Gs[hm_gram_at<L>(t, 16 * T)]);
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
             const float4 g = gr[q];
@@ -339,7 +419,7 @@ __global__ __launch_bounds__(hm_threads<L>(), 2) void hash_mm_kernel(const uint1
           ub |= (u ? 1u : 0u) << i;
           if (i < 15) {
             const float sg = u ? -1.f : 1.f;
-            const float4* gr = reinterpret_cast<const float4*>(&sh.Gs[hm_gram_row<L>(bit)]);
+            const float4* gr = reinterpret_cast<const float4*>(&sh.Gs[hm_gram_diag<L>(bit)]);
 #pragma unroll
             for (int q = (i + 1) / 4; q < 4; ++q) {
               const float4 g = gr[q];
