@@ -13,7 +13,7 @@
 // cut into three bf16 parts (hi + mid + lo, by truncation, exactly P), and
 // the products accumulate in fp32.  The corrections run in fp32 on the
 // vector units with the Gram matrix (fp64, rounded to fp32) as wavefront-
-// uniform operands; at L = 128 the corrections by earlier 16-bit blocks are
+// uniform operands; at L >= 64 the corrections by earlier 16-bit blocks are
 // one more bf16 contraction (signs +-1 times the Gram entries cut like P,
 // the hi products in a chain of their own) and only each block's own
 // triangle stays on the vector units.
@@ -151,13 +151,13 @@ __device__ __forceinline__ int hm_gram_row(int t) {
 template <int L>
 constexpr int hm_gram_size() { return 256 * (L / 16) * (L / 16 + 1) / 2; }
 
-// At L = 128 the corrections by earlier blocks run on the matrix cores (see
-// the main loop), and the Gram matrix (the same 36 KB) is kept as the 16 x 16
+// At L >= 64 the corrections by earlier blocks run on the matrix cores (see
+// the main loop), and the Gram matrix (the same size) is kept as the 16 x 16
 // diagonal blocks (row t, column i % 16 at 256 (t / 16) + 16 (t % 16) +
 // i % 16), then, for every bit i of block T >= 1, the 16 T entries G[t][i],
 // t < 16 T, contiguous (the matrix-core operand reads 8 consecutive t).
 template <int L>
-constexpr bool hm_mm_corr() { return L == 128; }
+constexpr bool hm_mm_corr() { return L >= 64; }
 template <int L>
 __device__ __forceinline__ int hm_gram_col(int i) {  // the entries G[t][i], t < 16 (i / 16)
   constexpr int nb = L / 16;
@@ -372,7 +372,7 @@ __global__ __launch_bounds__(hm_threads<L>(), 2) void hash_mm_kernel(const uint1
       }
       wave_lds_sync();
       // corrections by the bits of earlier blocks: y_j -= u_t Gr[t][j]
-      // (on the vector units below L = 128)
+      // (on the vector units at L = 32)
 #pragma unroll
       for (int w = 0; w < W; ++w) {
         if (hm_mm_corr<L>() || 32 * w >= 16 * T) break;
