@@ -93,8 +93,10 @@ def test_build_parity_tiny(tiny):
 
 @pytest.mark.parametrize("checkpoint", [False, True], ids=["recompute", "checkpoint"])
 # 33330 keys: 261 chunk sums of 128 keys, folded in blocks of 32 with a short
-# last block of 5 before the per-(b, h) tree
-@pytest.mark.parametrize("L,N,B,H", [(64, 1000, 2, 2), (128, 300, 1, 3), (32, 513, 1, 1), (64, 33330, 1, 1)])
+# last block of 5 before the per-(b, h) tree; 32769 keys: a last block of one
+# chunk sum holding one key
+@pytest.mark.parametrize("L,N,B,H", [(64, 1000, 2, 2), (128, 300, 1, 3), (32, 513, 1, 1), (64, 33330, 1, 1),
+                                     (32, 32769, 1, 1)])
 def test_build_parity_ragged_strided(L, N, B, H, checkpoint):
     announce(f"[build ragged] L={L} N={N} B={B} H={H} checkpoint={checkpoint}")
     rng = np.random.default_rng(L + N)
